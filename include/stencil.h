@@ -1,0 +1,154 @@
+/*
+ * stencil.h -- C ABI of the MI355X (gfx950) structured-grid stencil library.
+ *
+ * The operator is the one of the HIERA scientific-computing case study (experimental
+ * setup, paragraph "Case-study protocol"): a box stencil of radius R applied as a
+ * zero-padded cross-correlation with padding R and stride 1, repeated step after step on
+ * its own output, with per-step latency as the figure of merit.  This library computes
+ * that operator and its generalisations on one GPU:
+ *
+ *   one step   u_{t+1}[p] = k[p] * sum_{j} w_c[j] * u_t(p + O[j])      (k = 1 without field)
+ *   u_t(q)     = 0 outside the grid            (STENCIL_ZERO, re-applied at every step)
+ *              = u_t[q mod dims]               (STENCIL_PERIODIC, non-negative modulo)
+ *   result     = u_steps, written to `out`;   steps = 0 copies `in` to `out`.
+ *
+ * It is a cross-correlation: no flip of the weights (weight j multiplies u(p + O[j])).
+ * The coefficient field k, when present, is indexed by the OUTPUT point p.
+ *
+ * Layout.  Row-major (C order).  3D extents dims = {nz, ny, nx}, 2D dims = {ny, nx, -}; the
+ * last axis is unit-stride.  `batch` independent volumes are stored back to back (conv
+ * layout N x C x D x H x W gives batch = N * C); volume b uses weight set c = b % channels.
+ *
+ * Offset order O[j] (the order of each weight set):
+ *   STENCIL_BOX : lexicographic over (oz, oy, ox) in [-R, R]^3 (2D: (oy, ox)), ox fastest,
+ *                 i.e. a correlation kernel W[oz+R][oy+R][ox+R] flattened in C order;
+ *   STENCIL_STAR: the centre first, then for each axis from slowest to fastest the
+ *                 offsets -R..-1, +1..+R along that axis (1 + 2*ndim*R points).
+ *
+ * Arithmetic.  f32 grids are computed in fp32, f64 grids in fp64; the summation order
+ * and fused multiply-adds are the kernel's choice (results agree with an fp64 evaluation
+ * to within rounding).
+ *
+ * Errors.  Every call returns a stencil_status and never aborts.  All argument checks are
+ * made on the host before any HIP call, so invalid calls fail the same way on a machine
+ * without a GPU.  HIP failures return STENCIL_ERR_HIP.  A human-readable detail of the
+ * last failure on the calling thread is returned by stencil_last_error().
+ */
+#ifndef MI355X_STENCIL_H
+#define MI355X_STENCIL_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct stencil_plan_s *stencil_plan_t; /* opaque; created and freed by the library */
+
+typedef enum {
+    STENCIL_OK = 0,
+    STENCIL_ERR_INVALID_ARG = 1, /* NULL pointer, bad enum, non-positive extent, steps < 0 */
+    STENCIL_ERR_UNSUPPORTED = 2, /* radius or shape beyond the supported range, or a forced
+                                    variant that cannot run this description */
+    STENCIL_ERR_MISMATCH = 3,    /* apply() arguments disagree with the plan */
+    STENCIL_ERR_ALIAS = 4,       /* out overlaps in or the coefficient field */
+    STENCIL_ERR_NO_MEMORY = 5,   /* host or device allocation failed */
+    STENCIL_ERR_HIP = 6          /* a HIP runtime call failed (detail in stencil_last_error) */
+} stencil_status;
+
+typedef enum { STENCIL_F32 = 0, STENCIL_F64 = 1 } stencil_dtype;
+typedef enum { STENCIL_STAR = 0, STENCIL_BOX = 1 } stencil_shape;
+typedef enum { STENCIL_ZERO = 0, STENCIL_PERIODIC = 1 } stencil_boundary;
+
+/* Kernel families.  AUTO lets the planner choose; the others force one (for testing and
+ * tuning) and make stencil_plan() fail with STENCIL_ERR_UNSUPPORTED where it cannot run. */
+typedef enum {
+    STENCIL_VARIANT_AUTO = 0,
+    STENCIL_VARIANT_GENERIC = 1, /* one thread per point, any description */
+    STENCIL_VARIANT_STREAM = 2   /* 2.5D z-streaming tiles (3D, aligned x extent) */
+} stencil_variant;
+
+typedef struct {
+    int32_t ndim;            /* 2 or 3 */
+    int64_t dims[3];         /* slowest..fastest extents, each >= 1; 2D uses dims[0..1] */
+    int64_t batch;           /* number of contiguous volumes, >= 1 */
+    int32_t channels;        /* number of weight sets, >= 1; volume b uses set b % channels */
+    int32_t dtype;           /* stencil_dtype */
+    int32_t shape;           /* stencil_shape */
+    int32_t radius;          /* STAR: 0..4; BOX: 0..4 in 2D, 0..3 in 3D */
+    int32_t boundary;        /* stencil_boundary */
+    int32_t has_coeff_field; /* 1: out[p] = k[p] * sum_j w[j] * u(p + O[j]); 0: no field */
+    int32_t variant;         /* stencil_variant; 0 = AUTO */
+    int32_t temporal_depth;  /* steps fused per launch where the variant supports it;
+                                0 = planner's choice, 1 = one launch per step */
+} stencil_desc;
+
+typedef struct {
+    int32_t variant;         /* the stencil_variant chosen (never AUTO) */
+    int32_t temporal_depth;  /* steps fused per launch */
+    int64_t scratch_bytes;   /* device bytes the plan allocates for steps > 1 */
+    const char *kernel;      /* base name of the dominant GPU kernel (static string) */
+} stencil_plan_info;
+
+/*
+ * stencil_plan -- validate a description and create a plan for it.
+ *   desc      : host pointer, read during the call only.
+ *   out_plan  : receives the plan; set to NULL on failure.
+ * No HIP call is made here: device memory (coefficients, and the ping-pong grid used when
+ * steps > 1) is allocated by the first stencil_apply() that needs it, on the device current
+ * at that time, and the plan stays tied to that device.
+ * Returns STENCIL_OK, INVALID_ARG, UNSUPPORTED or NO_MEMORY.
+ */
+stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan);
+
+/*
+ * stencil_apply -- run `steps` steps of the planned operator on `stream`.
+ * (Operator: HIERA, "Case-study protocol"; generalisations as described at the top.)
+ *   plan        : from stencil_plan().
+ *   in          : device pointer, batch volumes of dims (dtype of the plan); read only.
+ *   out         : device pointer, same size; receives u_steps.  Must not overlap `in`.
+ *   dims        : host array {nz, ny, nx} (2D: {ny, nx, ignored}); must equal the plan's.
+ *   coeffs      : host pointer, channels * npoints weights of the plan's dtype, in the
+ *                 offset order above; copied before the call returns.
+ *   coeff_field : device pointer to one dims-shaped field per volume (same layout as `in`),
+ *                 or NULL; must be non-NULL exactly when the plan has a field.
+ *   radius, boundary : must equal the plan's (re-stated so a call reads as the operator).
+ *   steps       : >= 0.
+ *   stream      : HIP stream (NULL = default stream); all work is enqueued on it.
+ * Ownership: in, out and coeff_field belong to the caller and must stay valid until the
+ * stream work completes.  Asynchronous: returns once the work is enqueued.  Calls on one
+ * plan must be ordered on one stream at a time (the plan's ping-pong grid and coefficient
+ * buffer are reused).  Pointers or x extents that do not meet a fast kernel's alignment
+ * select a slower kernel; they are not an error.
+ * Returns STENCIL_OK, INVALID_ARG, MISMATCH, ALIAS, NO_MEMORY or ERR_HIP.
+ */
+stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
+                             const int64_t dims[3], const void *coeffs,
+                             const void *coeff_field, int32_t radius, int32_t boundary,
+                             int32_t steps, hipStream_t stream);
+
+/*
+ * stencil_destroy -- free a plan and its device memory.  NULL is accepted.  The caller
+ * must make sure no enqueued work still uses the plan (synchronise its stream first).
+ */
+stencil_status stencil_destroy(stencil_plan_t plan);
+
+/* Describe the plan's choices.  info: host pointer.  Returns OK or INVALID_ARG. */
+stencil_status stencil_plan_query(stencil_plan_t plan, stencil_plan_info *info);
+
+/* Number of offsets: STAR 1 + 2*ndim*R, BOX (2R+1)^ndim; -1 for an invalid description. */
+int32_t stencil_num_points(int32_t shape, int32_t ndim, int32_t radius);
+
+/* Static name of a status code ("STENCIL_OK", ...); "unknown status" otherwise. */
+const char *stencil_status_str(stencil_status status);
+
+/* Detail of the last failure on the calling thread ("" if none).  Valid until the next
+ * call on that thread. */
+const char *stencil_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MI355X_STENCIL_H */

@@ -1,0 +1,211 @@
+"""ctypes binding of ``libstencil.so`` (the C ABI declared in ``include/stencil.h``).
+
+Argument marshalling only: every step of the operator runs in the library's HIP kernels.
+The functions keep the C names (``stencil_plan``, ``stencil_apply``, ``stencil_destroy``,
+...) and raise ``StencilError`` on a non-OK status.  ``Plan`` and ``apply`` are thin
+conveniences over them for torch tensors (torch supplies device memory and streams).
+
+The library must have been built (``python -m paper_2608_21157_amd.build``); there is no
+fallback: loading fails loudly when it is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libstencil.so")
+
+# enums of stencil.h
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_MISMATCH, ERR_ALIAS, ERR_NO_MEMORY, ERR_HIP = range(7)
+F32, F64 = 0, 1
+STAR, BOX = 0, 1
+ZERO, PERIODIC = 0, 1
+VARIANT_AUTO, VARIANT_GENERIC, VARIANT_STREAM = 0, 1, 2
+VARIANT_NAMES = {VARIANT_GENERIC: "generic", VARIANT_STREAM: "stream"}
+
+EXPORTED = ("stencil_plan", "stencil_apply", "stencil_destroy", "stencil_plan_query",
+            "stencil_num_points", "stencil_status_str", "stencil_last_error")
+
+
+class StencilDesc(ctypes.Structure):
+    _fields_ = [("ndim", ctypes.c_int32), ("dims", ctypes.c_int64 * 3),
+                ("batch", ctypes.c_int64), ("channels", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("shape", ctypes.c_int32),
+                ("radius", ctypes.c_int32), ("boundary", ctypes.c_int32),
+                ("has_coeff_field", ctypes.c_int32), ("variant", ctypes.c_int32),
+                ("temporal_depth", ctypes.c_int32)]
+
+
+class StencilPlanInfo(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int32), ("temporal_depth", ctypes.c_int32),
+                ("scratch_bytes", ctypes.c_int64), ("kernel", ctypes.c_char_p)]
+
+
+class StencilError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(detail or "status %d" % status)
+        self.status = status
+
+
+_lib = None
+
+
+def load():
+    """Load ``libstencil.so`` and declare its signatures (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libstencil.so is not built (%s); run "
+                          "`python -m paper_2608_21157_amd.build` first" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp = ctypes.c_void_p
+    lib.stencil_plan.argtypes = [ctypes.POINTER(StencilDesc), ctypes.POINTER(vp)]
+    lib.stencil_plan.restype = ctypes.c_int
+    lib.stencil_apply.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_int64), vp, vp,
+                                  ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp]
+    lib.stencil_apply.restype = ctypes.c_int
+    lib.stencil_destroy.argtypes = [vp]
+    lib.stencil_destroy.restype = ctypes.c_int
+    lib.stencil_plan_query.argtypes = [vp, ctypes.POINTER(StencilPlanInfo)]
+    lib.stencil_plan_query.restype = ctypes.c_int
+    lib.stencil_num_points.argtypes = [ctypes.c_int32] * 3
+    lib.stencil_num_points.restype = ctypes.c_int32
+    lib.stencil_status_str.argtypes = [ctypes.c_int]
+    lib.stencil_status_str.restype = ctypes.c_char_p
+    lib.stencil_last_error.argtypes = []
+    lib.stencil_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise StencilError(status, load().stencil_last_error().decode())
+
+
+# ------------------------------------------------------------------ C names, marshalled
+
+def stencil_plan(desc: StencilDesc) -> int:
+    h = ctypes.c_void_p()
+    _check(load().stencil_plan(ctypes.byref(desc), ctypes.byref(h)))
+    return h.value
+
+
+def stencil_apply(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int | None,
+                  radius: int, boundary: int, steps: int, stream: int | None) -> None:
+    """``inp``/``out``/``coeff_field``: device addresses; ``coeffs``: a host buffer (numpy
+    array or ctypes pointer) of the plan's dtype; ``stream``: a hipStream_t handle."""
+    d = (ctypes.c_int64 * 3)(*(list(dims) + [0] * (3 - len(dims))))
+    cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
+    _check(load().stencil_apply(plan, inp, out, d, cp, coeff_field, radius, boundary, steps,
+                                stream))
+
+
+def stencil_destroy(plan: int | None) -> None:
+    _check(load().stencil_destroy(plan))
+
+
+def stencil_plan_query(plan: int) -> StencilPlanInfo:
+    info = StencilPlanInfo()
+    _check(load().stencil_plan_query(plan, ctypes.byref(info)))
+    return info
+
+
+def stencil_num_points(shape: int, ndim: int, radius: int) -> int:
+    return load().stencil_num_points(shape, ndim, radius)
+
+
+def stencil_status_str(status: int) -> str:
+    return load().stencil_status_str(status).decode()
+
+
+def stencil_last_error() -> str:
+    return load().stencil_last_error().decode()
+
+
+# ------------------------------------------------------------------ torch conveniences
+
+def make_desc(ndim, dims, *, batch=1, channels=1, dtype=F32, shape=STAR, radius=1,
+              boundary=ZERO, has_coeff_field=False, variant=VARIANT_AUTO,
+              temporal_depth=0) -> StencilDesc:
+    d = StencilDesc()
+    d.ndim = ndim
+    for i, v in enumerate(list(dims)[:3]):
+        d.dims[i] = int(v)
+    d.batch, d.channels, d.dtype, d.shape = int(batch), int(channels), int(dtype), int(shape)
+    d.radius, d.boundary, d.has_coeff_field = int(radius), int(boundary), int(bool(has_coeff_field))
+    d.variant, d.temporal_depth = int(variant), int(temporal_depth)
+    return d
+
+
+class Plan:
+    """Owns a ``stencil_plan_t``; ``run`` calls ``stencil_apply`` on torch tensors."""
+
+    def __init__(self, desc: StencilDesc):
+        self.desc = desc
+        self.handle = stencil_plan(desc)
+        self.dims = tuple(desc.dims[i] for i in range(desc.ndim))
+        self._stream = None
+
+    def info(self) -> StencilPlanInfo:
+        return stencil_plan_query(self.handle)
+
+    def run(self, x, y, coeffs, *, steps: int, field=None, stream=None) -> None:
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        sh = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+        self._stream = stream
+        stencil_apply(self.handle, x.data_ptr(), y.data_ptr(), self.dims, coeffs,
+                      None if field is None else field.data_ptr(), self.desc.radius,
+                      self.desc.boundary, steps, sh)
+
+    def close(self) -> None:
+        """Wait for the last stream this plan ran on, then free the plan."""
+        if self.handle:
+            if self._stream is not None and hasattr(self._stream, "synchronize"):
+                self._stream.synchronize()
+            stencil_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def apply(x, y, coeffs, *, shape: int, radius: int, boundary: int = ZERO, steps: int = 1,
+          field=None, ndim: int | None = None, channels: int = 1, variant: int = VARIANT_AUTO,
+          temporal_depth: int = 0, stream=None) -> None:
+    """One-shot: plan, apply and destroy.  ``x``, ``y`` (and ``field``): contiguous CUDA
+    tensors of shape (*dims), (batch, *dims) or (N, C, *dims), float32 or float64;
+    ``coeffs``: host numpy array (channels, npoints) of the same dtype."""
+    import numpy as np
+    import torch
+    if not (x.is_cuda and y.is_cuda and x.is_contiguous() and y.is_contiguous()):
+        raise ValueError("x and y must be contiguous device tensors")
+    if x.dtype != y.dtype or x.shape != y.shape:
+        raise ValueError("x and y must have the same dtype and shape")
+    if field is not None and (not field.is_cuda or not field.is_contiguous()
+                              or field.dtype != x.dtype or field.shape != x.shape):
+        raise ValueError("field must be a contiguous device tensor shaped like x")
+    dt = {torch.float32: F32, torch.float64: F64}.get(x.dtype)
+    if dt is None:
+        raise ValueError("float32 or float64 tensors only")
+    if ndim is None:
+        ndim = 3 if x.dim() >= 3 else 2
+    lead = x.shape[: x.dim() - ndim]
+    batch = int(np.prod(lead)) if len(lead) else 1
+    c = np.ascontiguousarray(coeffs, dtype=np.float32 if dt == F32 else np.float64)
+    desc = make_desc(ndim, x.shape[x.dim() - ndim:], batch=batch, channels=channels, dtype=dt,
+                     shape=shape, radius=radius, boundary=boundary,
+                     has_coeff_field=field is not None, variant=variant,
+                     temporal_depth=temporal_depth)
+    p = Plan(desc)
+    try:
+        p.run(x, y, c, steps=steps, field=field, stream=stream)
+    finally:
+        p.close()

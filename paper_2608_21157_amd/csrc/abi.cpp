@@ -1,0 +1,346 @@
+// abi.cpp -- the C ABI of the stencil library: argument validation, plan lifetime,
+// coefficient upload and the step loop (ping-pong between `out` and the plan's grid).
+//
+// The operator is the iterated zero-padded cross-correlation of the HIERA case study
+// (experimental setup, "Case-study protocol"), generalised as documented in stencil.h.
+// Every check below runs on the host before the first HIP call of an entry point.
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "plan.hpp"
+
+using stencil::Geometry;
+using stencil::Plan;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+stencil_status fail(stencil_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = std::string(stencil_status_str(st)) + ": " + buf;
+    return st;
+}
+
+stencil_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(STENCIL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int32_t points(int32_t shape, int32_t ndim, int32_t radius)
+{
+    if ((ndim != 2 && ndim != 3) || radius < 0)
+        return -1;
+    if (shape == STENCIL_STAR)
+        return 1 + 2 * ndim * radius;
+    if (shape == STENCIL_BOX) {
+        int32_t side = 2 * radius + 1;
+        return ndim == 2 ? side * side : side * side * side;
+    }
+    return -1;
+}
+
+// Largest grid handled: element offsets are 64-bit, but each volume must stay below 2^31
+// elements so that in-volume indices fit the kernels' 32-bit arithmetic.
+constexpr int64_t kMaxVolume = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxElements = int64_t(1) << 40;
+
+stencil_status validate_desc(const stencil_desc *d, Geometry *g)
+{
+    if (d == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "desc is NULL");
+    if (d->ndim != 2 && d->ndim != 3)
+        return fail(STENCIL_ERR_INVALID_ARG, "ndim must be 2 or 3 (got %d)", d->ndim);
+    for (int a = 0; a < d->ndim; ++a)
+        if (d->dims[a] < 1)
+            return fail(STENCIL_ERR_INVALID_ARG, "dims[%d] must be >= 1 (got %lld)", a,
+                        (long long)d->dims[a]);
+    if (d->batch < 1)
+        return fail(STENCIL_ERR_INVALID_ARG, "batch must be >= 1");
+    if (d->channels < 1)
+        return fail(STENCIL_ERR_INVALID_ARG, "channels must be >= 1");
+    if (d->dtype != STENCIL_F32 && d->dtype != STENCIL_F64)
+        return fail(STENCIL_ERR_INVALID_ARG, "unknown dtype %d", d->dtype);
+    if (d->shape != STENCIL_STAR && d->shape != STENCIL_BOX)
+        return fail(STENCIL_ERR_INVALID_ARG, "unknown shape %d", d->shape);
+    if (d->boundary != STENCIL_ZERO && d->boundary != STENCIL_PERIODIC)
+        return fail(STENCIL_ERR_INVALID_ARG, "unknown boundary %d", d->boundary);
+    if (d->has_coeff_field != 0 && d->has_coeff_field != 1)
+        return fail(STENCIL_ERR_INVALID_ARG, "has_coeff_field must be 0 or 1");
+    if (d->radius < 0)
+        return fail(STENCIL_ERR_INVALID_ARG, "radius must be >= 0");
+    if (d->temporal_depth < 0)
+        return fail(STENCIL_ERR_INVALID_ARG, "temporal_depth must be >= 0");
+    if (d->variant < STENCIL_VARIANT_AUTO || d->variant > STENCIL_VARIANT_STREAM)
+        return fail(STENCIL_ERR_INVALID_ARG, "unknown variant %d", d->variant);
+    const int rmax = (d->shape == STENCIL_STAR) ? 4 : (d->ndim == 2 ? 4 : 3);
+    if (d->radius > rmax)
+        return fail(STENCIL_ERR_UNSUPPORTED, "radius %d exceeds %d for this shape", d->radius,
+                    rmax);
+
+    g->ndim = d->ndim;
+    g->nz = (d->ndim == 3) ? d->dims[0] : 1;
+    g->ny = (d->ndim == 3) ? d->dims[1] : d->dims[0];
+    g->nx = (d->ndim == 3) ? d->dims[2] : d->dims[1];
+    if (g->nz > kMaxVolume || g->ny > kMaxVolume || g->nx > kMaxVolume)
+        return fail(STENCIL_ERR_UNSUPPORTED, "extent too large");
+    g->vol = g->nz * g->ny * g->nx;
+    if (g->vol / g->nx / g->ny != g->nz || g->vol > kMaxVolume)
+        return fail(STENCIL_ERR_UNSUPPORTED, "volume exceeds 2^31-1 elements");
+    if (d->batch > kMaxElements / g->vol)
+        return fail(STENCIL_ERR_UNSUPPORTED, "batch * volume exceeds 2^40 elements");
+    g->batch = d->batch;
+    g->channels = d->channels;
+    g->npts = points(d->shape, d->ndim, d->radius);
+    g->shape = d->shape;
+    g->radius = d->radius;
+    g->boundary = d->boundary;
+    g->field = d->has_coeff_field != 0;
+    g->dtype = d->dtype;
+    g->elt = (d->dtype == STENCIL_F32) ? 4 : 8;
+    return STENCIL_OK;
+}
+
+bool overlaps(const void *a, const void *b, size_t bytes)
+{
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + bytes && pb < pa + bytes;
+}
+
+bool aligned16(const void *p)
+{
+    return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *stencil_status_str(stencil_status s)
+{
+    switch (s) {
+    case STENCIL_OK: return "STENCIL_OK";
+    case STENCIL_ERR_INVALID_ARG: return "STENCIL_ERR_INVALID_ARG";
+    case STENCIL_ERR_UNSUPPORTED: return "STENCIL_ERR_UNSUPPORTED";
+    case STENCIL_ERR_MISMATCH: return "STENCIL_ERR_MISMATCH";
+    case STENCIL_ERR_ALIAS: return "STENCIL_ERR_ALIAS";
+    case STENCIL_ERR_NO_MEMORY: return "STENCIL_ERR_NO_MEMORY";
+    case STENCIL_ERR_HIP: return "STENCIL_ERR_HIP";
+    }
+    return "unknown status";
+}
+
+const char *stencil_last_error(void)
+{
+    return g_last_error.c_str();
+}
+
+int32_t stencil_num_points(int32_t shape, int32_t ndim, int32_t radius)
+{
+    return points(shape, ndim, radius);
+}
+
+stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan)
+{
+    if (out_plan == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    Geometry g{};
+    stencil_status st = validate_desc(desc, &g);
+    if (st != STENCIL_OK)
+        return st;
+
+    int variant = desc->variant;
+    const bool stream_ok = stencil::stream_supported(g);
+    if (variant == STENCIL_VARIANT_AUTO)
+        variant = stream_ok ? STENCIL_VARIANT_STREAM : STENCIL_VARIANT_GENERIC;
+    if (variant == STENCIL_VARIANT_STREAM && !stream_ok)
+        return fail(STENCIL_ERR_UNSUPPORTED,
+                    "the streaming kernels need a 3D grid with a supported shape and radius "
+                    "and an x extent they can tile");
+    const int max_depth = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_max_depth(g) : 1;
+    int depth = desc->temporal_depth == 0 ? max_depth : desc->temporal_depth;
+    if (depth > max_depth)
+        return fail(STENCIL_ERR_UNSUPPORTED, "temporal_depth %d exceeds %d for this variant",
+                    desc->temporal_depth, max_depth);
+
+    Plan *p = new (std::nothrow) Plan();
+    if (p == nullptr)
+        return fail(STENCIL_ERR_NO_MEMORY, "plan allocation failed");
+    p->desc = *desc;
+    p->geo = g;
+    p->variant = variant;
+    p->depth = depth;
+    p->kernel = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_kernel_name(g)
+                                                    : "stencil_generic_kernel";
+    p->scratch_bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
+    *out_plan = reinterpret_cast<stencil_plan_t>(p);
+    g_last_error.clear();
+    return STENCIL_OK;
+}
+
+stencil_status stencil_plan_query(stencil_plan_t plan, stencil_plan_info *info)
+{
+    if (plan == nullptr || info == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "plan or info is NULL");
+    const Plan *p = reinterpret_cast<const Plan *>(plan);
+    info->variant = p->variant;
+    info->temporal_depth = p->depth;
+    info->scratch_bytes = int64_t(p->scratch_bytes);
+    info->kernel = p->kernel;
+    return STENCIL_OK;
+}
+
+stencil_status stencil_destroy(stencil_plan_t plan)
+{
+    if (plan == nullptr)
+        return STENCIL_OK;
+    Plan *p = reinterpret_cast<Plan *>(plan);
+    stencil_status st = STENCIL_OK;
+    if (p->device >= 0) {
+        int cur = -1;
+        if (hipGetDevice(&cur) == hipSuccess && cur != p->device)
+            (void)hipSetDevice(p->device);
+        if (p->stage_done && hipEventSynchronize(p->stage_done) != hipSuccess)
+            st = STENCIL_ERR_HIP;
+        if (p->stage_done)
+            (void)hipEventDestroy(p->stage_done);
+        if (p->h_stage)
+            (void)hipHostFree(p->h_stage);
+        if (p->d_coeff)
+            (void)hipFree(p->d_coeff);
+        if (p->scratch)
+            (void)hipFree(p->scratch);
+        if (cur >= 0 && cur != p->device)
+            (void)hipSetDevice(cur);
+    }
+    delete p;
+    if (st != STENCIL_OK)
+        return fail(st, "event synchronisation failed while destroying the plan");
+    return STENCIL_OK;
+}
+
+stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
+                             const int64_t dims[3], const void *coeffs,
+                             const void *coeff_field, int32_t radius, int32_t boundary,
+                             int32_t steps, hipStream_t stream)
+{
+    // ---- host-only validation ------------------------------------------------------
+    if (plan == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "plan is NULL");
+    Plan *p = reinterpret_cast<Plan *>(plan);
+    const Geometry &g = p->geo;
+    if (in == nullptr || out == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "in and out must be non-NULL device pointers");
+    if (coeffs == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "coeffs must be a host pointer");
+    if (dims == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "dims is NULL");
+    if (steps < 0)
+        return fail(STENCIL_ERR_INVALID_ARG, "steps must be >= 0 (got %d)", steps);
+    for (int a = 0; a < g.ndim; ++a)
+        if (dims[a] != p->desc.dims[a])
+            return fail(STENCIL_ERR_MISMATCH, "dims[%d] = %lld, plan has %lld", a,
+                        (long long)dims[a], (long long)p->desc.dims[a]);
+    if (radius != g.radius)
+        return fail(STENCIL_ERR_MISMATCH, "radius %d, plan has %d", radius, g.radius);
+    if (boundary != g.boundary)
+        return fail(STENCIL_ERR_MISMATCH, "boundary %d, plan has %d", boundary, g.boundary);
+    if ((coeff_field != nullptr) != g.field)
+        return fail(STENCIL_ERR_MISMATCH, g.field ? "the plan needs a coefficient field"
+                                                  : "the plan has no coefficient field");
+    const size_t bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
+    if (overlaps(in, out, bytes))
+        return fail(STENCIL_ERR_ALIAS, "out overlaps in");
+    if (coeff_field != nullptr && overlaps(coeff_field, out, bytes))
+        return fail(STENCIL_ERR_ALIAS, "out overlaps the coefficient field");
+
+    // fast kernels use 16-byte vector accesses; misaligned pointers run the generic kernel
+    const bool fast = p->variant == STENCIL_VARIANT_STREAM && aligned16(in) && aligned16(out) &&
+                      (coeff_field == nullptr || aligned16(coeff_field));
+    const int depth = fast ? p->depth : 1;
+    const int launches = (steps + depth - 1) / depth;
+
+    // ---- device state (first use) --------------------------------------------------
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (p->device >= 0 && dev != p->device)
+        return fail(STENCIL_ERR_MISMATCH, "plan belongs to device %d, current device is %d",
+                    p->device, dev);
+    p->device = dev;
+    const size_t wbytes = size_t(g.channels) * size_t(g.npts) * g.elt;
+    if (p->d_coeff == nullptr) {
+        if ((e = hipMalloc(&p->d_coeff, wbytes)) != hipSuccess) {
+            p->d_coeff = nullptr;
+            return fail(STENCIL_ERR_NO_MEMORY, "hipMalloc(%zu) for weights: %s", wbytes,
+                        hipGetErrorString(e));
+        }
+        if ((e = hipHostMalloc(&p->h_stage, wbytes, hipHostMallocDefault)) != hipSuccess) {
+            p->h_stage = nullptr;
+            return fail(STENCIL_ERR_NO_MEMORY, "hipHostMalloc(%zu): %s", wbytes,
+                        hipGetErrorString(e));
+        }
+        if ((e = hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming)) != hipSuccess) {
+            p->stage_done = nullptr;
+            return hip_fail(e, "hipEventCreateWithFlags");
+        }
+        p->h_cache.assign(wbytes, 0);
+    }
+    if (launches > 1 && p->scratch == nullptr) {
+        if ((e = hipMalloc(&p->scratch, p->scratch_bytes)) != hipSuccess) {
+            p->scratch = nullptr;
+            return fail(STENCIL_ERR_NO_MEMORY, "hipMalloc(%zu) for the ping-pong grid: %s",
+                        p->scratch_bytes, hipGetErrorString(e));
+        }
+    }
+    // ---- weights: upload only when they changed --------------------------------------
+    if (!p->coeff_valid || std::memcmp(p->h_cache.data(), coeffs, wbytes) != 0) {
+        if ((e = hipEventSynchronize(p->stage_done)) != hipSuccess)
+            return hip_fail(e, "hipEventSynchronize(staging)");
+        std::memcpy(p->h_stage, coeffs, wbytes);
+        if ((e = hipMemcpyAsync(p->d_coeff, p->h_stage, wbytes, hipMemcpyHostToDevice,
+                                stream)) != hipSuccess)
+            return hip_fail(e, "hipMemcpyAsync(weights)");
+        if ((e = hipEventRecord(p->stage_done, stream)) != hipSuccess)
+            return hip_fail(e, "hipEventRecord(staging)");
+        std::memcpy(p->h_cache.data(), coeffs, wbytes);
+        p->coeff_valid = true;
+    }
+
+    // ---- steps ------------------------------------------------------------------------
+    if (steps == 0) {
+        if ((e = hipMemcpyAsync(out, in, bytes, hipMemcpyDeviceToDevice, stream)) != hipSuccess)
+            return hip_fail(e, "hipMemcpyAsync(copy for steps = 0)");
+        return STENCIL_OK;
+    }
+    // launch i writes `out` when an even number of launches follows it, so the last one
+    // always lands in `out`; launch i > 0 reads what launch i - 1 wrote
+    const void *src = in;
+    int left = steps;
+    for (int i = 0; i < launches; ++i) {
+        const int d = left < depth ? left : depth;
+        void *dst = ((launches - 1 - i) % 2 == 0) ? out : p->scratch;
+        if (fast)
+            e = stencil::launch_stream(g, src, dst, coeff_field, p->d_coeff, d, stream);
+        else
+            e = stencil::launch_generic(g, src, dst, coeff_field, p->d_coeff, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "kernel launch");
+        src = dst;
+        left -= d;
+    }
+    return STENCIL_OK;
+}
+
+}  // extern "C"

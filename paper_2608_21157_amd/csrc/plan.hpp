@@ -1,0 +1,60 @@
+// plan.hpp -- internal plan state and kernel launchers of the stencil library.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "stencil.h"
+
+namespace stencil {
+
+// Geometry of one apply: every extent is the 3D view (nz = 1 for a 2D grid).
+struct Geometry {
+    int ndim;
+    int64_t nz, ny, nx;
+    int64_t vol;      // nz * ny * nx
+    int64_t batch;
+    int channels;
+    int npts;
+    int shape;        // STENCIL_STAR / STENCIL_BOX
+    int radius;
+    int boundary;     // STENCIL_ZERO / STENCIL_PERIODIC
+    bool field;
+    int dtype;        // STENCIL_F32 / STENCIL_F64
+    size_t elt;       // bytes per element
+};
+
+struct Plan {
+    stencil_desc desc{};
+    Geometry geo{};
+    int variant = STENCIL_VARIANT_GENERIC;
+    int depth = 1;                 // steps fused per launch
+    const char *kernel = "";
+
+    int device = -1;               // device of the first apply
+    void *d_coeff = nullptr;       // channels * npts weights (device)
+    void *h_stage = nullptr;       // pinned staging of the weights
+    hipEvent_t stage_done = nullptr;
+    std::vector<unsigned char> h_cache;  // weights last uploaded
+    bool coeff_valid = false;
+    void *scratch = nullptr;       // ping-pong grid for steps > 1
+    size_t scratch_bytes = 0;
+};
+
+// Launch one pass of `depth` steps (depth <= plan.depth) from src to dst.  `w` is the
+// device weight buffer (channels * npts of the plan's dtype).
+hipError_t launch_generic(const Geometry &g, const void *src, void *dst, const void *field,
+                          const void *w, hipStream_t stream);
+
+// 2.5D z-streaming kernels.  `supported` says whether the kernel family can run a
+// geometry (shape, radius, alignment of the x extent); launch_* run one pass.
+bool stream_supported(const Geometry &g);
+int stream_max_depth(const Geometry &g);
+const char *stream_kernel_name(const Geometry &g);
+hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const void *field,
+                         const void *w, int depth, hipStream_t stream);
+
+}  // namespace stencil

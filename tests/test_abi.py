@@ -1,0 +1,159 @@
+"""The C ABI on the CPU: exports, validation and status codes, with no GPU work.
+
+Every check in ``stencil_plan``/``stencil_apply`` happens on the host before the first HIP
+call, so invalid calls are tested here with placeholder device addresses that the library
+never dereferences.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_21157_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "stencil.h")
+
+IN, OUT, FIELD = 0x7F0000000000, 0x7F0100000000, 0x7F0200000000  # never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(stencil_\w+)\s*\(", text)))
+
+
+def desc3(**kw):
+    base = dict(batch=1, channels=1, dtype=B.F32, shape=B.STAR, radius=1, boundary=B.ZERO)
+    base.update(kw)
+    dims = base.pop("dims", (8, 8, 8))
+    return B.make_desc(3, dims, **base)
+
+
+def status_of(fn, *args):
+    try:
+        fn(*args)
+    except B.StencilError as e:
+        return e.status
+    return B.OK
+
+
+def test_library_exports_every_declared_function():
+    lib = B.load()
+    declared = header_functions()
+    assert set(declared) == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_point_counts():
+    assert B.stencil_status_str(B.OK) == "STENCIL_OK"
+    assert B.stencil_status_str(B.ERR_ALIAS) == "STENCIL_ERR_ALIAS"
+    assert B.stencil_status_str(99) == "unknown status"
+    assert B.stencil_num_points(B.STAR, 3, 4) == 25
+    assert B.stencil_num_points(B.BOX, 3, 1) == 27
+    assert B.stencil_num_points(B.BOX, 2, 3) == 49
+    assert B.stencil_num_points(B.STAR, 2, 1) == 5
+    assert B.stencil_num_points(B.STAR, 4, 1) == -1
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dims=(0, 8, 8)), B.ERR_INVALID_ARG),
+    (dict(batch=0), B.ERR_INVALID_ARG),
+    (dict(channels=0), B.ERR_INVALID_ARG),
+    (dict(dtype=2), B.ERR_INVALID_ARG),
+    (dict(shape=5), B.ERR_INVALID_ARG),
+    (dict(boundary=3), B.ERR_INVALID_ARG),
+    (dict(radius=-1), B.ERR_INVALID_ARG),
+    (dict(radius=5), B.ERR_UNSUPPORTED),
+    (dict(shape=B.BOX, radius=4), B.ERR_UNSUPPORTED),
+    (dict(variant=7), B.ERR_INVALID_ARG),
+    (dict(temporal_depth=-1), B.ERR_INVALID_ARG),
+    (dict(variant=B.VARIANT_GENERIC, temporal_depth=2), B.ERR_UNSUPPORTED),
+    (dict(dims=(1 << 11, 1 << 11, 1 << 11)), B.ERR_UNSUPPORTED),
+])
+def test_plan_rejects(kw, status):
+    assert status_of(B.stencil_plan, desc3(**kw)) == status
+    assert B.stencil_status_str(status) in B.stencil_last_error()
+
+
+def test_plan_rejects_bad_ndim_and_null():
+    d = desc3()
+    d.ndim = 4
+    assert status_of(B.stencil_plan, d) == B.ERR_INVALID_ARG
+    h = ctypes.c_void_p(123)
+    assert B.load().stencil_plan(None, ctypes.byref(h)) == B.ERR_INVALID_ARG
+    assert h.value is None
+    assert B.load().stencil_plan(ctypes.byref(desc3()), None) == B.ERR_INVALID_ARG
+
+
+def test_forced_stream_variant_needs_3d():
+    d2 = B.make_desc(2, (64, 64), variant=B.VARIANT_STREAM)
+    assert status_of(B.stencil_plan, d2) == B.ERR_UNSUPPORTED
+
+
+def test_plan_and_query_without_gpu():
+    h = B.stencil_plan(B.make_desc(2, (16, 16), shape=B.BOX, radius=3, dtype=B.F64))
+    info = B.stencil_plan_query(h)
+    assert info.variant == B.VARIANT_GENERIC and info.temporal_depth == 1
+    assert info.scratch_bytes == 16 * 16 * 8
+    assert info.kernel.decode() == "stencil_generic_kernel"
+    B.stencil_destroy(h)
+    B.stencil_destroy(None)
+
+
+@pytest.fixture
+def plan():
+    h = B.stencil_plan(desc3(dims=(4, 5, 6), shape=B.BOX, radius=1, has_coeff_field=True))
+    yield h
+    B.stencil_destroy(h)
+
+
+W27 = np.zeros(27, np.float32)
+
+
+def apply_status(h, inp=IN, out=OUT, dims=(4, 5, 6), coeffs=W27, field=FIELD, radius=1,
+                 boundary=B.ZERO, steps=1):
+    return status_of(B.stencil_apply, h, inp, out, dims, coeffs, field, radius, boundary, steps,
+                     None)
+
+
+def test_apply_validation(plan):
+    assert apply_status(None) == B.ERR_INVALID_ARG
+    assert apply_status(plan, inp=None) == B.ERR_INVALID_ARG
+    assert apply_status(plan, out=None) == B.ERR_INVALID_ARG
+    assert apply_status(plan, coeffs=None) == B.ERR_INVALID_ARG
+    assert apply_status(plan, steps=-1) == B.ERR_INVALID_ARG
+    assert apply_status(plan, dims=(4, 5, 7)) == B.ERR_MISMATCH
+    assert apply_status(plan, radius=2) == B.ERR_MISMATCH
+    assert apply_status(plan, boundary=B.PERIODIC) == B.ERR_MISMATCH
+    assert apply_status(plan, field=None) == B.ERR_MISMATCH
+    assert apply_status(plan, out=IN) == B.ERR_ALIAS
+    assert apply_status(plan, out=IN + 4 * 100) == B.ERR_ALIAS         # partial overlap
+    assert apply_status(plan, out=IN + 4 * 120) != B.ERR_ALIAS         # just past the end
+    assert apply_status(plan, out=FIELD + 8) == B.ERR_ALIAS
+    assert "overlaps" in B.stencil_last_error()
+    d = (ctypes.c_int64 * 3)(4, 5, 6)
+    assert B.load().stencil_apply(plan, IN, OUT, None, W27.ctypes.data, FIELD, 1, 0, 1,
+                                  None) == B.ERR_INVALID_ARG
+    assert B.load().stencil_apply(plan, IN, OUT, d, W27.ctypes.data, None, 1, 0, 1,
+                                  None) == B.ERR_MISMATCH
+
+
+def test_field_given_to_plan_without_field():
+    h = B.stencil_plan(desc3(dims=(4, 5, 6)))
+    try:
+        assert apply_status(h, coeffs=np.zeros(7, np.float32)) == B.ERR_MISMATCH
+    finally:
+        B.stencil_destroy(h)
+
+
+def test_valid_apply_without_gpu_reports_hip_error(plan):
+    """All checks pass, then the first HIP call fails cleanly on a host with no GPU."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert apply_status(plan) == B.ERR_HIP
+    assert "hipGetDevice" in B.stencil_last_error()

@@ -1,0 +1,180 @@
+"""GPU parity: the HIP library (through the C ABI) against the fp64 CPU oracle.
+
+Reduced sizes (several tiles and ragged tails in every axis) are compared element by
+element with the full oracle; the full workload sizes are compared on sampled points that
+the oracle evaluates one by one (corners, points within R*steps of a face, random points),
+plus properties that hold at any size (finite values, the norm bound).
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_21157_amd import binding as B
+from paper_2608_21157_amd import inputs
+from paper_2608_21157_amd.inputs import WORKLOADS
+from parity_util import (gather, oracle_full, report, run_library, sample_points, tolerance)
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = [B.VARIANT_AUTO, B.VARIANT_GENERIC]
+
+REDUCED = [
+    ("c1", (256, 256), None, None),
+    ("c1", (37, 61), None, None),
+    ("c2", (40, 36, 72), None, None),
+    ("c2", (33, 19, 20), None, 3),
+    ("c3", (24, 40, 264), None, None),
+    ("c3", (17, 23, 520), None, 1),
+    ("c4", (20, 18, 520), None, None),
+    ("c4", (9, 13, 256), None, None),
+    ("c5", (20, 24, 128), 2, None),
+    ("c5b", (12, 10, 128), 1, None),
+    ("paper", (300, 260), None, 3),
+]
+
+
+def _case(name, dims, n, steps):
+    wl = WORKLOADS[name].resized(dims, n=n, steps=steps)
+    return wl, inputs.make(wl)
+
+
+@pytest.mark.parametrize("variant", VARIANTS, ids=["auto", "generic"])
+@pytest.mark.parametrize("name,dims,n,steps", REDUCED,
+                         ids=["%s-%s" % (r[0], "x".join(map(str, r[1]))) for r in REDUCED])
+def test_reduced_size_parity(name, dims, n, steps, variant):
+    wl, (x, w, k) = _case(name, dims, n, steps)
+    print("[case] %s dims=%s steps=%d variant=%d" % (name, dims, wl.steps, variant), flush=True)
+    got, info = run_library(wl, x, w, k, variant=variant)
+    ref = oracle_full(wl, x, w, k)
+    report("%s %s %s" % (name, dims, info), got, ref, tolerance(wl, x, k))
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c5b"])
+def test_full_size_sampled_parity(name):
+    wl = WORKLOADS[name]
+    print("[case] full %s dims=%s batch=%d steps=%d" % (name, wl.dims, wl.batch, wl.steps),
+          flush=True)
+    x, w, k = inputs.make(wl)
+    got, info = run_library(wl, x, w, k)
+    print("[info] %s" % info, flush=True)
+    pts = sample_points(wl, x, 400, seed=1)
+    ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                              steps=wl.steps, field=k, ndim=wl.ndim, channels=wl.channels)
+    tol = tolerance(wl, x, k)
+    report("full %s (%d samples)" % (name, len(pts)), gather(got, pts, wl), ref, tol)
+    # property at every point: |S^s x| <= (max k * sum|w|)^s * max|x|
+    gain = float(np.abs(w.astype(np.float64)).sum(axis=1).max())
+    if k is not None:
+        gain *= float(k.max())
+    bound = gain ** wl.steps * float(np.abs(x).max())
+    assert np.isfinite(got).all()
+    assert float(np.abs(got).max()) <= bound * (1 + 1e-5) + tol
+
+
+@pytest.mark.parametrize("steps", [0, 1, 2, 3, 4, 5])
+@pytest.mark.parametrize("name", ["c2", "c3", "c4"])
+def test_steps_and_ping_pong(name, steps):
+    wl, (x, w, k) = _case(name, (14, 21, 264) if name != "c4" else (11, 9, 256), None, steps)
+    got, _ = run_library(wl, x, w, k, steps=steps)
+    ref = oracle_full(wl, x, w, k, steps=steps)
+    report("%s steps=%d" % (name, steps), got, ref, tolerance(wl, x, k, steps))
+    if steps == 0:
+        assert np.array_equal(got, x.astype(np.float64))
+
+
+TINY = [(1, 1, 1), (1, 2, 3), (2, 4, 9), (3, 1, 4), (5, 6, 7), (9, 3, 8)]
+
+
+@pytest.mark.parametrize("dims", TINY)
+@pytest.mark.parametrize("shape,R", [(B.STAR, 4), (B.BOX, 1), (B.BOX, 3), (B.STAR, 1)])
+@pytest.mark.parametrize("boundary", [B.ZERO, B.PERIODIC])
+def test_tiny_grids(dims, shape, R, boundary):
+    g = np.random.default_rng(3)
+    wl = WORKLOADS["c4"].resized(dims)
+    from dataclasses import replace
+    wl = replace(wl, shape=shape, radius=R, boundary=boundary, steps=2, has_field=False)
+    x = g.uniform(-1, 1, dims).astype(np.float32)
+    w = g.uniform(-1, 1, (1, wl.npoints))
+    w = (w / np.abs(w).sum()).astype(np.float32)
+    got, _ = run_library(wl, x, w)
+    ref = oracle_full(wl, x, w)
+    report("tiny %s shape=%d R=%d bnd=%d" % (dims, shape, R, boundary), got, ref,
+           tolerance(wl, x))
+
+
+def test_input_untouched_and_guard_band():
+    """`in` is not modified; NaN guard cells around `out` stay NaN."""
+    wl, (x, w, k) = _case("c4", (10, 12, 256), None, None)
+    dev = torch.device("cuda:0")
+    xt = torch.from_numpy(x).to(dev)
+    kt = torch.from_numpy(k).to(dev)
+    n = x.size
+    pad = 4096
+    buf = torch.full((n + 2 * pad,), float("nan"), dtype=xt.dtype, device=dev)
+    y = buf[pad:pad + n].view(x.shape)
+    B.apply(xt, y, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary, steps=1,
+            field=kt, ndim=3)
+    torch.cuda.synchronize()
+    assert torch.isnan(buf[:pad]).all() and torch.isnan(buf[pad + n:]).all()
+    assert np.array_equal(xt.cpu().numpy(), x)
+    ref = oracle_full(wl, x, w, k)
+    report("guard", y.cpu().numpy().astype(np.float64), ref, tolerance(wl, x, k))
+
+
+def test_misaligned_pointers_fall_back():
+    """Pointers off the 16-byte grid run a scalar kernel and still match."""
+    wl, (x, w, k) = _case("c3", (12, 14, 264), None, 2)
+    dev = torch.device("cuda:0")
+    n = x.size
+    bx = torch.zeros(n + 1, dtype=torch.float32, device=dev)
+    by = torch.zeros(n + 1, dtype=torch.float32, device=dev)
+    xt = bx[1:].view(x.shape)
+    xt.copy_(torch.from_numpy(x).to(dev))
+    yt = by[1:].view(x.shape)
+    B.apply(xt, yt, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary, steps=2, ndim=3)
+    torch.cuda.synchronize()
+    ref = oracle_full(wl, x, w, k, steps=2)
+    report("misaligned", yt.cpu().numpy().astype(np.float64), ref, tolerance(wl, x, steps=2))
+
+
+def test_plan_reuse_with_changing_weights():
+    """One plan, two weight sets in a row on one stream: each call sees its own weights."""
+    wl, (x, w, k) = _case("c4", (8, 9, 256), None, None)
+    dev = torch.device("cuda:0")
+    xt = torch.from_numpy(x).to(dev)
+    kt = torch.from_numpy(k).to(dev)
+    desc = B.make_desc(3, x.shape, shape=wl.shape, radius=1, boundary=wl.boundary,
+                       has_coeff_field=True)
+    plan = B.Plan(desc)
+    try:
+        outs = []
+        w2 = (-w[:, ::-1]).copy()
+        for ww in (w, w2, w):
+            y = torch.empty_like(xt)
+            plan.run(xt, y, ww, steps=1, field=kt)
+            outs.append((ww, y))
+        torch.cuda.synchronize()
+        for ww, y in outs:
+            ref = oracle_full(wl, x, ww, k)
+            report("reuse", y.cpu().numpy().astype(np.float64), ref, tolerance(wl, x, k))
+    finally:
+        plan.close()
+
+
+def test_nondefault_stream():
+    wl, (x, w, k) = _case("c3", (16, 20, 264), None, 3)
+    s = torch.cuda.Stream()
+    got, _ = run_library(wl, x, w, k, stream=s)
+    ref = oracle_full(wl, x, w, k)
+    report("stream", got, ref, tolerance(wl, x, k))
+
+
+def test_variants_agree():
+    """Every variant the planner can force gives the oracle's result on the same input."""
+    wl, (x, w, k) = _case("c4", (16, 20, 512), None, None)
+    ref = oracle_full(wl, x, w, k)
+    for variant in (B.VARIANT_GENERIC, B.VARIANT_AUTO):
+        got, info = run_library(wl, x, w, k, variant=variant)
+        report("variant %s" % info, got, ref, tolerance(wl, x, k))
