@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Throughput of the MI355X stencil library on its headline workload, one GPU.
+
+A step is one ``stencil_apply`` of the headline workload: the 25-point radius-4 star
+(8th-order Laplacian weights) on a 512^3 fp32 grid, zero boundary, 4 stencil steps per
+call, inputs already resident in HBM.  The metric is stencil points per second
+(Gpoints/s = 512^3 * 4 / time per call) with the achieved HBM bandwidth of the dominant
+kernel against the compulsory-traffic roofline (each point read once and written once
+per stencil step: 8 bytes per point-step in fp32).
+
+Prints one JSON line on stdout; progress goes to stderr.  Besides the headline it reports
+every other workload (2D 5-point, 3D 7-point x10, 27-point box with a coefficient field
+(periodic), depthwise 3x3x3 conv form in fp32 and fp64), a copy-probe ceiling, and the
+CPU oracle timed on a bounded slab of the headline input.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = {
+    "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp"],
+    "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp"],
+    "stencil_generic_kernel": ["kernel_generic.hip"],
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha(kernel: str) -> str | None:
+    files = KERNEL_SOURCES.get(kernel)
+    if not files:
+        return None
+    h = hashlib.sha256()
+    for f in files:
+        path = os.path.join(ROOT, "paper_2608_21157_amd", "csrc", f)
+        if not os.path.exists(path):
+            return None
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel: str, workload: str, algo_bytes: float):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None when
+    the summary is missing or the kernel source changed since it was taken."""
+    path = os.path.join(PROFILES, "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get("%s/%s" % (kernel, workload))
+    if not rec or rec.get("source_sha") != kernel_source_sha(kernel):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+class Runner:
+    def __init__(self, torch, B, inputs, wl, stream):
+        self.torch, self.B, self.wl, self.stream = torch, B, wl, stream
+        import numpy as np
+        t0 = time.perf_counter()
+        x, w, k = inputs.make(wl)
+        log("[bench] %s: inputs generated in %.1fs" % (wl.name, time.perf_counter() - t0))
+        self.x_host = x
+        dev = torch.device("cuda:0")
+        self.x = torch.from_numpy(x).to(dev)
+        self.y = torch.empty_like(self.x)
+        self.k = None if k is None else torch.from_numpy(k).to(dev)
+        self.w = np.ascontiguousarray(w)
+        desc = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
+                           dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
+                           radius=wl.radius, boundary=wl.boundary,
+                           has_coeff_field=self.k is not None)
+        self.plan = B.Plan(desc)
+        info = self.plan.info()
+        self.kernel = info.kernel.decode()
+        self.depth = info.temporal_depth
+        self.variant = B.VARIANT_NAMES.get(info.variant, str(info.variant))
+        self.launches = math.ceil(wl.steps / self.depth) if wl.steps else 0
+
+    def call(self):
+        self.plan.run(self.x, self.y, self.w, steps=self.wl.steps, field=self.k,
+                      stream=self.stream)
+
+    def timed(self, K: int, W: int) -> float:
+        """Milliseconds for K back-to-back calls (events on the launch stream)."""
+        torch = self.torch
+        for _ in range(W):
+            self.call()
+        self.stream.synchronize()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for _ in range(K):
+            self.call()
+        e1.record(self.stream)
+        e1.synchronize()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    def flushed(self, R: int, flush) -> list:
+        """Per-call milliseconds with L2 and the Infinity Cache flushed before each call
+        (the flush runs on the same stream, outside the events)."""
+        torch = self.torch
+        out = []
+        for i in range(R):
+            flush.fill_(float(i))
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            self.call()
+            e1.record(self.stream)
+            e1.synchronize()
+            out.append(e0.elapsed_time(e1))
+        return out
+
+    def close(self):
+        self.plan.close()
+        del self.x, self.y, self.k
+
+
+def figures(wl, ms_per_call: float) -> dict:
+    pts = wl.points_per_step * wl.steps
+    bytes_pt = wl.itemsize * (2 + (1 if wl.has_field else 0))
+    gpts = pts / (ms_per_call * 1e-3) / 1e9
+    gbs = pts * bytes_pt / (ms_per_call * 1e-3) / 1e9
+    return {"ms_per_call": round(ms_per_call, 5), "gpoints_per_s": round(gpts, 2),
+            "effective_gbs": round(gbs, 1), "frac_of_8tbs": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
+    path = os.path.join(ROOT, "paper_2608_21157_amd", "libstencil_probe.so")
+    lib = ctypes.CDLL(path)
+    lib.stencil_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                       ctypes.c_void_p]
+    lib.stencil_probe_copy.restype = ctypes.c_int
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").uniform_()
+    b = torch.empty_like(a)
+    sh = stream.cuda_stream
+    for _ in range(3):
+        assert lib.stencil_probe_copy(a.data_ptr(), b.data_ptr(), nbytes, sh) == 0
+    stream.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        lib.stencil_probe_copy(a.data_ptr(), b.data_ptr(), nbytes, sh)
+    e1.record(stream)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    assert torch.equal(a, b)
+    del a, b
+    return {"bytes": nbytes, "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}
+
+
+def cpu_baseline(wl, x_host, w, planes: int):
+    """The fp64 oracle, single-threaded, on a z-slab of the headline input."""
+    import oracle
+    oracle.build()
+    slab = x_host[:planes]
+    t0 = time.perf_counter()
+    oracle.apply(slab, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                 steps=wl.steps, ndim=wl.ndim)
+    dt = time.perf_counter() - t0
+    pts = slab.size * wl.steps
+    return {"value": round(pts / dt / 1e9, 6), "unit": "Gpoints/s", "cores": 1,
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": "%dx%dx%d z-slab of the headline input, %d steps, fp64 single thread"
+                      % (slab.shape + (wl.steps,))}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20, help="timed calls")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed calls")
+    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-others", action="store_true", help="headline workload only")
+    ap.add_argument("--cpu-planes", type=int, default=24)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        log("bench.py measures one GPU only: this library runs the stencil on a single "
+            "MI355X (multi-GPU slab decomposition is a design note, not built).  "
+            "Use --gpus 1.")
+        return 2
+
+    import torch
+    from paper_2608_21157_amd import binding as B
+    from paper_2608_21157_amd import inputs
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        return 1
+    B.load()
+    stream = torch.cuda.Stream()
+    wl = inputs.WORKLOADS[args.workload]
+
+    head = Runner(torch, B, inputs, wl, stream)
+    ms_total = head.timed(args.steps, args.warmup)
+    ms = ms_total / args.steps
+    fig = figures(wl, ms)
+    launches = head.launches * args.steps
+    bytes_pt = wl.itemsize * (2 + (1 if wl.has_field else 0))
+    algo_per_launch = wl.points_per_step * (wl.steps / head.launches) * bytes_pt
+    avg_launch_ms = ms_total / launches
+    achieved = algo_per_launch / (avg_launch_ms * 1e-3) / 1e9
+    traffic = counter_traffic(head.kernel, wl.name, algo_per_launch)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": head.kernel,
+                "avg_launch_ms": round(avg_launch_ms, 5),
+                "algorithmic_bytes_per_launch": int(algo_per_launch)}
+    log("[bench] %s: %.4f ms/call, %.1f Gpoints/s, %.1f GB/s (%.1f%% of 8 TB/s)" % (
+        wl.name, ms, fig["gpoints_per_s"], achieved, 100 * achieved / HBM_PEAK_GBS))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, head.x_host, head.w, args.cpu_planes)
+        log("[bench] cpu oracle: %s" % cpu)
+    head.close()
+    torch.cuda.empty_cache()
+
+    others = {}
+    probe = None
+    if not args.no_others:
+        probe = copy_probe(torch, stream)
+        log("[bench] copy probe: %s" % probe)
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0")  # 1 GiB
+        for name in ("c1", "c2", "c3", "c4", "c5", "c5b"):
+            w2 = inputs.WORKLOADS[name]
+            r = Runner(torch, B, inputs, w2, stream)
+            t = r.timed(20, 3) / 20
+            fl = r.flushed(10, flush)
+            rec = figures(w2, t)
+            rec["flushed_median_ms"] = round(statistics.median(fl), 5)
+            rec["flushed_gpoints_per_s"] = figures(w2, statistics.median(fl))["gpoints_per_s"]
+            rec.update(kernel=r.kernel, variant=r.variant, depth=r.depth,
+                       launches_per_call=r.launches)
+            if probe:
+                rec["frac_of_copy_probe"] = round(rec["effective_gbs"] / probe["gbs"], 4)
+            others[name] = rec
+            log("[bench] %s: %s" % (name, rec))
+            r.close()
+            torch.cuda.empty_cache()
+        del flush
+
+    line = {
+        "metric": "stencil Gpoints/s and achieved HBM GB/s (% of MI355X peak), 3D fp32 512^3",
+        "value": fig["gpoints_per_s"], "unit": "Gpoints/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded: 8 random-phase sinusoids + 1% uniform noise)",
+        "config": {"workload": "3D 25-point star R=4 (8th-order Laplacian, sum|w|=1), "
+                               "512^3 fp32, zero boundary, 4 steps per call",
+                   "dims": list(wl.dims), "stencil_steps_per_call": wl.steps,
+                   "kernel": head.kernel, "variant": head.variant,
+                   "temporal_depth": head.depth, "parallelism": "single GPU"},
+        "effective_gbs": fig["effective_gbs"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "copy_probe": probe,
+        "workloads": others,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -66,7 +66,9 @@ typedef enum { STENCIL_ZERO = 0, STENCIL_PERIODIC = 1 } stencil_boundary;
 typedef enum {
     STENCIL_VARIANT_AUTO = 0,
     STENCIL_VARIANT_GENERIC = 1, /* one thread per point, any description */
-    STENCIL_VARIANT_STREAM = 2   /* 2.5D z-streaming tiles (3D, aligned x extent) */
+    STENCIL_VARIANT_STREAM = 2   /* tiled kernels: 3D 3x3x3 box and 2D/3D stars up to radius
+                                    4, 2.5D z-streaming in 3D; x extent a multiple of 16
+                                    bytes (box: whole 64-lane row segments) */
 } stencil_variant;
 
 typedef struct {

@@ -1,0 +1,34 @@
+/*
+ * stencil_probe.h -- HBM copy probe used to calibrate the stencil measurements.
+ *
+ * The stencil kernels are judged against the compulsory-traffic roofline (each input
+ * element read once, each output element written once).  This probe measures what a
+ * plain streaming copy achieves on the same device, so that the stencil figures can be
+ * read against both the nominal HBM peak and an achievable ceiling, and so that hardware
+ * byte counters can be scaled by what they read for a copy of known size.
+ */
+#ifndef MI355X_STENCIL_PROBE_H
+#define MI355X_STENCIL_PROBE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * stencil_probe_copy -- copy `bytes` bytes from `src` to `dst` on `stream` with 16-byte
+ * vector loads and stores, one grid-stride kernel launch.
+ *   src, dst : device pointers, 16-byte aligned, non-overlapping (caller-owned).
+ *   bytes    : a multiple of 16, >= 0.
+ * Asynchronous.  Returns 0 on success, 1 for invalid arguments (checked on the host
+ * before any HIP call), 2 if the launch failed.
+ */
+int stencil_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MI355X_STENCIL_PROBE_H */

@@ -1,0 +1,342 @@
+// kernel_box.hip -- 27-point (3x3x3 box, radius 1) stencil, 2.5D z-streaming, gfx950.
+//
+// Computes one step of out[p] = (k[p] *) sum_o w[o] * in[p + o] over the 27 offsets
+// o in [-1, 1]^3 (cross-correlation, HIERA "Case-study protocol", generalised to 3D with
+// an output-indexed coefficient field, zero or periodic boundary, and batched volumes
+// with per-channel weights).
+//
+// Mapping (no LDS, no barriers):
+//   * a wavefront owns a row segment of 64 lanes x 16 bytes (256 floats / 128 doubles)
+//     along x -- or, for narrower rows, 64/lpr whole rows side by side -- times TY rows
+//     per lane along y, and streams a chunk of z planes;
+//   * every input plane is read once per wavefront as TY + 2 coalesced 16-byte row loads
+//     per lane (the two extra rows are the y halo, shared through L2 with the wave that
+//     owns them);
+//   * x neighbours come from the adjacent lanes through DPP wave shifts; only the first
+//     and last lane of a segment load the one-element x halo;
+//   * each input row is folded into three rotating accumulator planes (the outputs at
+//     z_in - 1, z_in, z_in + 1), so the completed plane z_in - 1 is written as soon as
+//     plane z_in has been read;
+//   * each row register is reloaded with the next plane right after its last use, so
+//     the loads of plane z_in + 1 are in flight while plane z_in is folded in;
+//   * loads and stores use buffer resources: 32-bit offsets, and rows outside the grid
+//     take an offset past the resource, which reads zero (the zero padding) and drops
+//     stores.
+// Workgroups are 4 wavefronts stacked along y; their order is renumbered per XCD.
+#include "common.hpp"
+#include "plan.hpp"
+
+#include <cstdlib>
+
+namespace stencil {
+namespace {
+
+struct BoxParams {
+    int nz, ny, nx;
+    long long vol;
+    int lpr;        // lanes per row segment, 2..64
+    int segw;       // x extent of a segment = lpr * elements per 16 bytes
+    int segs;       // segments per row
+    int rows_wave;  // output rows per wavefront = (64 / lpr) * TY
+    int ywaves;     // wavefront row blocks per volume
+    int ygroups;    // workgroup row blocks per volume (4 wavefronts each)
+    int zc, nzc;    // z planes per chunk, chunks per volume
+    int channels;
+    int nblocks;
+};
+
+template <typename T>
+__device__ __forceinline__ T madd(T a, T b, T c)
+{
+    return fma(a, b, c);
+}
+
+template <typename T, int TY, bool PERIODIC, bool FIELD>
+__global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
+    const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ field,
+    const T *__restrict__ w, BoxParams p)
+{
+    constexpr int VEC = Vec16<T>::N;
+    constexpr int NR = TY + 2;  // input rows per lane and plane
+    constexpr int E = sizeof(T);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+
+    int t = xcd_logical_block(blockIdx.x, p.nblocks);
+    const int yg = t % p.ygroups;
+    t /= p.ygroups;
+    const int zi = t % p.nzc;
+    t /= p.nzc;
+    const int seg = t % p.segs;
+    const long long b = t / p.segs;
+    const int yw = yg * 4 + wave;
+    if (yw >= p.ywaves)
+        return;  // whole wavefront leaves; the kernel has no barriers
+
+    const int lx = lane % p.lpr;
+    const int rg = lane / p.lpr;
+    const int x = seg * p.segw + lx * VEC;
+    const int y0 = yw * p.rows_wave + rg * TY;
+    const int z0 = zi * p.zc;
+    const int n = min(p.zc, p.nz - z0);  // output planes of this chunk
+    const long long plane = (long long)p.ny * p.nx;
+    const unsigned plane_bytes = unsigned(plane * E);
+    const T *src = in + b * p.vol;
+    T *dst = out + b * p.vol;
+    const T *kf = FIELD ? field + b * p.vol : nullptr;
+    const T *wb = w + (b % p.channels) * 27;
+    T W[27];
+#pragma unroll
+    for (int j = 0; j < 27; ++j)
+        W[j] = wb[j];
+
+    // byte offsets of input rows y0 - 1 .. y0 + TY within a plane; rows outside the grid
+    // (zero boundary) get an offset past the resource and read as zero
+    const bool first = lx == 0, last = lx == p.lpr - 1;
+    int hx = first ? seg * p.segw - 1 : seg * p.segw + p.segw;
+    bool hok = (first || last) && hx >= 0 && hx < p.nx;
+    if (PERIODIC) {
+        hx = wrap_index(hx, p.nx);
+        hok = first || last;
+    }
+    int ro[NR], ho[NR];
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+        int yi = y0 - 1 + i;
+        bool ok = yi >= 0 && yi < p.ny;
+        if (PERIODIC) {
+            yi = wrap_index(yi, p.ny);
+            ok = true;
+        }
+        ro[i] = ok ? (yi * p.nx + x) * E : kOutOfRange;
+        ho[i] = (ok && hok) ? (yi * p.nx + hx) * E : kOutOfRange;
+    }
+
+    // resource of input plane z_in; under the zero boundary a plane outside the grid
+    // gets zero records, so every load from it returns zero
+    auto plane_rsrc = [&](int zin) {
+        bool zok = zin >= 0 && zin < p.nz;
+        if (PERIODIC) {
+            zin = wrap_index(zin, p.nz);
+            zok = true;
+        }
+        return make_rsrc(src + (zok ? zin : 0) * plane, zok ? plane_bytes : 0u);
+    };
+
+    T acc[3][TY][VEC];
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+#pragma unroll
+        for (int o = 0; o < TY; ++o)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[s][o][e] = T(0);
+
+    Vec16<T> rows[NR];
+    T halo[NR];
+    Vec16<T> kv[TY];
+    {
+        const auto r0 = plane_rsrc(z0 - 1);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            rows[i] = bload16<T>(r0, ro[i]);
+            halo[i] = bload1(r0, ho[i], T(0));
+        }
+    }
+    auto load_field = [&](int q) {
+        if (FIELD) {
+            const auto rk = make_rsrc(kf + (long long)(z0 + q) * plane, plane_bytes);
+#pragma unroll
+            for (int o = 0; o < TY; ++o)
+                kv[o] = bload16<T>(rk, ((y0 + o) * p.nx + x) * E);
+        }
+    };
+
+    // Fold input plane k (z_in = z0 - 1 + k) into the accumulators, reloading each row
+    // register with the next plane right after its last use.  Offset (a, bb, c) in weight
+    // order is (oz, oy, ox) = (a - 1, bb - 1, c - 1); the input point feeds output plane
+    // q = k - a (slot q mod 3) and output row o = i - bb.  Planes outside [0, n) are
+    // skipped.
+    auto fold = [&](int k, auto slot_of_a) {
+        const bool more = k + 1 <= n + 1;
+        const auto rn = plane_rsrc(z0 + k);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            T r[VEC + 2];
+            const T left = from_left_lane(rows[i].e[VEC - 1], halo[i]);
+            const T right = from_right_lane(rows[i].e[0], halo[i]);
+            r[0] = first ? halo[i] : left;
+            r[VEC + 1] = last ? halo[i] : right;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                r[e + 1] = rows[i].e[e];
+            if (more) {
+                rows[i] = bload16<T>(rn, ro[i]);
+                halo[i] = bload1(rn, ho[i], T(0));
+            }
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+                if (k - a < 0 || k - a >= n)
+                    continue;  // uniform
+                const int s = slot_of_a(a);
+#pragma unroll
+                for (int bb = 0; bb < 3; ++bb) {
+                    const int o = i - bb;
+                    if (o < 0 || o >= TY)
+                        continue;  // resolved at compile time
+                    const T w0 = W[a * 9 + bb * 3 + 0], w1 = W[a * 9 + bb * 3 + 1],
+                            w2 = W[a * 9 + bb * 3 + 2];
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        T v = acc[s][o][e];
+                        v = madd(w0, r[e], v);
+                        v = madd(w1, r[e + 1], v);
+                        v = madd(w2, r[e + 2], v);
+                        acc[s][o][e] = v;
+                    }
+                }
+            }
+        }
+    };
+
+    // write output plane q from slot s (rows past the grid fall outside the resource and
+    // are dropped) and clear the slot; the field rows are read here rather than prefetched,
+    // which keeps the kernel at three wavefronts per SIMD
+    auto emit = [&](int q, int s) {
+        const auto rd = make_rsrc(dst + (long long)(z0 + q) * plane, plane_bytes);
+        load_field(q);
+#pragma unroll
+        for (int o = 0; o < TY; ++o) {
+            Vec16<T> v;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                v.e[e] = FIELD ? acc[s][o][e] * kv[o].e[e] : acc[s][o][e];
+            const int yo = y0 + o;
+            bstore16<T>(rd, yo < p.ny ? (yo * p.nx + x) * E : kOutOfRange, v);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[s][o][e] = T(0);
+        }
+    };
+
+    // prologue: planes k = 0, 1 (no output plane completes yet)
+    fold(0, [](int a) { return (3 - a) % 3; });
+    fold(1, [](int a) { return (4 - a) % 3; });
+
+    // steady state: plane k = 2 + 3m + j completes output plane q = k - 2 (slot j)
+    for (int k0 = 2; k0 <= n + 1; k0 += 3) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            const int k = k0 + j;
+            if (k > n + 1)
+                break;
+            fold(k, [j](int a) { return (2 + j - a + 3) % 3; });
+            emit(k - 2, j);
+        }
+    }
+}
+
+template <typename T>
+constexpr int vec_of()
+{
+    return Vec16<T>::N;
+}
+
+int lanes_per_row(const Geometry &g, int vec)
+{
+    if (g.nx % vec != 0)
+        return 0;
+    const int64_t nxv = g.nx / vec;
+    if (nxv >= 64)
+        return (nxv % 64 == 0) ? 64 : 0;
+    return (nxv >= 2 && 64 % nxv == 0) ? int(nxv) : 0;
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *s = std::getenv(name);
+    return (s && *s) ? std::atoi(s) : dflt;
+}
+
+template <typename T, int TY>
+BoxParams make_params(const Geometry &g)
+{
+    constexpr int VEC = Vec16<T>::N;
+    BoxParams p{};
+    p.nz = int(g.nz);
+    p.ny = int(g.ny);
+    p.nx = int(g.nx);
+    p.vol = g.vol;
+    p.lpr = lanes_per_row(g, VEC);
+    p.segw = p.lpr * VEC;
+    p.segs = p.nx / p.segw;
+    p.rows_wave = (64 / p.lpr) * TY;
+    p.ywaves = (p.ny + p.rows_wave - 1) / p.rows_wave;
+    p.ygroups = (p.ywaves + 3) / 4;
+    p.channels = g.channels;
+    const long long base = g.batch * p.segs * p.ygroups;
+    // enough workgroups to fill 256 CUs several times over; at least 8 planes per chunk
+    const long long target = env_int("STENCIL_BOX_TARGET_BLOCKS", 1024);
+    long long nzc = (target + base - 1) / base;
+    const long long max_chunks = (p.nz + 7) / 8;
+    if (nzc > max_chunks)
+        nzc = max_chunks;
+    if (nzc < 1)
+        nzc = 1;
+    p.zc = int((p.nz + nzc - 1) / nzc);
+    const int zc_env = env_int("STENCIL_BOX_ZC", 0);
+    if (zc_env > 0)
+        p.zc = zc_env < p.nz ? zc_env : p.nz;
+    p.nzc = (p.nz + p.zc - 1) / p.zc;
+    p.nblocks = int(base * p.nzc);
+    return p;
+}
+
+template <typename T, int TY>
+hipError_t launch_ty(const Geometry &g, const void *src, void *dst, const void *field,
+                     const void *w, hipStream_t stream)
+{
+    const BoxParams p = make_params<T, TY>(g);
+    const T *s = static_cast<const T *>(src);
+    T *d = static_cast<T *>(dst);
+    const T *k = static_cast<const T *>(field);
+    const T *wt = static_cast<const T *>(w);
+    const dim3 grid(p.nblocks), block(256);
+    const bool per = g.boundary == STENCIL_PERIODIC;
+    if (per && g.field)
+        stencil_box3_stream_kernel<T, TY, true, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    else if (per)
+        stencil_box3_stream_kernel<T, TY, true, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    else if (g.field)
+        stencil_box3_stream_kernel<T, TY, false, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    else
+        stencil_box3_stream_kernel<T, TY, false, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool box_stream_supported(const Geometry &g)
+{
+    if (g.ndim != 3 || g.shape != STENCIL_BOX || g.radius != 1)
+        return false;
+    const int vec = (g.dtype == STENCIL_F32) ? 4 : 2;
+    if (lanes_per_row(g, vec) == 0)
+        return false;
+    // in-plane byte offsets must stay below the out-of-range marker; block counts fit int
+    return g.ny * g.nx * int64_t(g.elt) < (int64_t(1) << 30) &&
+           g.batch * (g.nx / vec) * g.ny < (int64_t(1) << 30);
+}
+
+hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, const void *field,
+                             const void *w, hipStream_t stream)
+{
+    const int ty = env_int("STENCIL_BOX_TY", 8);
+    if (g.dtype == STENCIL_F32)
+        return ty == 4 ? launch_ty<float, 4>(g, src, dst, field, w, stream)
+                       : launch_ty<float, 8>(g, src, dst, field, w, stream);
+    return ty == 4 ? launch_ty<double, 4>(g, src, dst, field, w, stream)
+                   : launch_ty<double, 8>(g, src, dst, field, w, stream);
+}
+
+}  // namespace stencil

@@ -1,0 +1,389 @@
+// kernel_star.hip -- star stencils of radius R <= 4 (1 + 6R points in 3D, 1 + 4R in 2D),
+// 2.5D z-streaming with an LDS plane tile, gfx950.
+//
+// Computes one step of out[p] = sum_j w[j] * u(p + O[j]) over the star offsets (centre,
+// then -R..-1, +1..+R along z, y and x) -- the operator of the HIERA case study ("Case-
+// study protocol": zero-padded cross-correlation, stride 1), generalised to star offset
+// sets, periodic wrap and batched volumes.
+//
+// Mapping:
+//   * a workgroup (4 wavefronts) owns a TXW x TYW tile of the x-y plane and streams a
+//     chunk of z planes; a lane owns a 16-byte vector along x times TY rows along y;
+//   * z neighbours: every lane keeps the 2R + 1 planes around the current one for its own
+//     points in registers (a queue of 2R + 2 slots, one of them the prefetched next
+//     plane), so each input point is loaded from HBM once per chunk;
+//   * x and y neighbours: the current plane is staged in LDS with an R-row halo above and
+//     below and a whole-vector halo left and right (corners are never read by a star and
+//     are not loaded); the halo is loaded one plane ahead into registers;
+//   * LDS is double-buffered, one barrier per plane;
+//   * consecutive z chunks of a column stream in opposite directions, so the R planes two
+//     chunks share are read by both at about the same time (from L2, not twice from HBM);
+//   * global accesses use buffer resources with 32-bit offsets; cells outside the grid
+//     read zero (zero boundary) and stores outside the grid are dropped.
+#include "common.hpp"
+#include "plan.hpp"
+
+#include <cstdlib>
+
+namespace stencil {
+namespace {
+
+constexpr int kLanesX = 16;                  // lanes along x in a row group
+constexpr int kRowGroups = 64 / kLanesX;     // row groups per wavefront
+constexpr int kWaves = 4;
+
+struct StarParams {
+    int nz, ny, nx;
+    long long vol;
+    int ntx, nty;   // tiles along x and y
+    int zc, nzc;    // planes per z chunk, chunks
+    int nblocks;
+    int channels;
+};
+
+template <typename T, int R, int TY, bool ZAXIS>
+struct StarShape {
+    static constexpr int VEC = Vec16<T>::N;
+    static constexpr int TXW = kLanesX * VEC;
+    static constexpr int TYW = kWaves * kRowGroups * TY;
+    static constexpr int HX = ((R + VEC - 1) / VEC) * VEC;  // x halo in whole vectors
+    static constexpr int LDW = TXW + 2 * HX;                // LDS row pitch (elements)
+    static constexpr int LDH = TYW + 2 * R;
+    static constexpr int NQ = ZAXIS ? 2 * R + 2 : 1;        // queue slots
+    static constexpr int NBUF = ZAXIS ? 2 : 1;
+    // halo vectors per plane: R rows above and below (tile width), HX columns left/right
+    static constexpr int HTB = 2 * R * (TXW / VEC);
+    static constexpr int HLR = 2 * TYW * (HX / VEC);
+    static constexpr int NH = (HTB + HLR + 255) / 256;      // halo vectors per thread
+};
+
+template <typename T, int R, int TY, bool PERIODIC, bool ZAXIS>
+__global__ __launch_bounds__(256) void stencil_star_stream_kernel(
+    const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, StarParams p)
+{
+    using S = StarShape<T, R, TY, ZAXIS>;
+    constexpr int VEC = S::VEC, TXW = S::TXW, TYW = S::TYW, HX = S::HX, LDW = S::LDW;
+    constexpr int NQ = S::NQ, NH = S::NH;
+    constexpr int E = sizeof(T);
+    constexpr int RZ = ZAXIS ? R : 0;
+    __shared__ Vec16<T> lds_raw[S::NBUF][S::LDH * LDW / VEC];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    int t = xcd_logical_block(blockIdx.x, p.nblocks);
+    const int tx = t % p.ntx;
+    t /= p.ntx;
+    const int ty = t % p.nty;
+    t /= p.nty;
+    const int zi = t % p.nzc;
+    const long long b = t / p.nzc;
+    const int x0 = tx * TXW, y0 = ty * TYW;
+    const int lxi = lane % kLanesX, rgi = lane / kLanesX;
+    const int strip = (wave * kRowGroups + rgi) * TY;  // first own row within the tile
+    const int x = x0 + lxi * VEC;
+    const long long plane = (long long)p.ny * p.nx;
+    const unsigned plane_bytes = unsigned(plane * E);
+    const T *src = in + b * p.vol;
+    T *dst = out + b * p.vol;
+
+    // byte offset of the vector at grid row gy, column gx (a multiple of VEC): wrapped
+    // under the periodic boundary, past the resource (reads zero) under the zero one
+    auto goff = [&](int gy, int gx) {
+        if (PERIODIC) {
+            gy = wrap_index(gy, p.ny);
+            gx = wrap_index(gx, p.nx);
+            return (gy * p.nx + gx) * E;
+        }
+        return (gy >= 0 && gy < p.ny && gx >= 0 && gx < p.nx) ? (gy * p.nx + gx) * E
+                                                               : kOutOfRange;
+    };
+    int own[TY], sto[TY];
+#pragma unroll
+    for (int o = 0; o < TY; ++o) {
+        const int gy = y0 + strip + o;
+        own[o] = goff(gy, x);
+        sto[o] = (gy < p.ny && x < p.nx) ? (gy * p.nx + x) * E : kOutOfRange;
+    }
+    // halo vectors of this thread: global offset and LDS vector index (-1: none)
+    int hoff[NH], hlds[NH];
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+        const int idx = tid + 256 * h;
+        int ly = 0, lc = 0;
+        hlds[h] = -1;
+        hoff[h] = kOutOfRange;
+        if (idx < S::HTB) {
+            const int r = idx / (TXW / VEC);
+            ly = r < R ? r : TYW + r;
+            lc = HX + (idx % (TXW / VEC)) * VEC;
+            hlds[h] = (ly * LDW + lc) / VEC;
+        } else if (idx < S::HTB + S::HLR) {
+            const int j = idx - S::HTB;
+            const int per_row = 2 * (HX / VEC);
+            const int k = j % per_row;
+            ly = R + j / per_row;
+            lc = (k < HX / VEC) ? k * VEC : TXW + k * VEC;  // left block, or right block
+            hlds[h] = (ly * LDW + lc) / VEC;
+        }
+        if (hlds[h] >= 0)
+            hoff[h] = goff(y0 + ly - R, x0 + lc - HX);
+    }
+
+    // weights: z by queue position (direction-aware), y and x by offset
+    const T *wb = w + (b % p.channels) * (1 + 2 * (ZAXIS ? 3 : 2) * R);
+    const int dir = (ZAXIS && (zi & 1)) ? -1 : 1;
+    T wz[2 * RZ + 1], wy[2 * R], wx[2 * R];
+    wz[RZ] = wb[0];
+    int j = 1;
+    if (ZAXIS) {
+#pragma unroll
+        for (int i = 0; i < 2 * R; ++i) {
+            // weight index i is offset -R..-1, +1..+R; queue position of offset oz is
+            // R + dir * oz
+            const int oz = i < R ? i - R : i - R + 1;
+            const int pos = R + dir * oz;
+            // written with a select so that the array index stays static
+#pragma unroll
+            for (int q = 0; q < 2 * R + 1; ++q)
+                if (q == pos)
+                    wz[q] = wb[1 + i];
+        }
+        j += 2 * R;
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * R; ++i)
+        wy[i] = wb[j + i];
+#pragma unroll
+    for (int i = 0; i < 2 * R; ++i)
+        wx[i] = wb[j + 2 * R + i];
+
+    const int z0 = zi * p.zc;
+    const int n = min(p.zc, p.nz - z0);
+    const int zs = dir > 0 ? z0 : z0 + n - 1;
+
+    auto plane_rsrc = [&](int z) {
+        bool ok = z >= 0 && z < p.nz;
+        if (PERIODIC) {
+            z = wrap_index(z, p.nz);
+            ok = true;
+        }
+        return make_rsrc(src + (ok ? z : 0) * plane, ok ? plane_bytes : 0u);
+    };
+
+    Vec16<T> Q[NQ][TY];
+    Vec16<T> hreg[NH];
+    // prologue: queue positions 0 .. 2R + 1 hold planes zs + dir * (i - R); halo of zs
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) {
+        const auto rq = plane_rsrc(zs + dir * (i - RZ));
+#pragma unroll
+        for (int o = 0; o < TY; ++o)
+            Q[i][o] = bload16<T>(rq, own[o]);
+    }
+    {
+        const auto rh = plane_rsrc(zs);
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+            hreg[h] = bload16<T>(rh, hoff[h]);
+    }
+
+    // one plane: iteration m (phase = m mod NQ) computes output plane zs + dir * m
+    auto step = [&](int m, int phase) {
+        const int zc = zs + dir * m;
+        Vec16<T> *buf = lds_raw[ZAXIS ? (phase & 1) : 0];
+        // stage the current plane: own rows (queue position R) and the halo
+#pragma unroll
+        for (int o = 0; o < TY; ++o)
+            buf[((R + strip + o) * LDW + HX + lxi * VEC) / VEC] = Q[(phase + RZ) % NQ][o];
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+            if (hlds[h] >= 0)
+                buf[hlds[h]] = hreg[h];
+        if (ZAXIS && m + 1 < n) {
+            const auto rh = plane_rsrc(zc + dir);
+#pragma unroll
+            for (int h = 0; h < NH; ++h)
+                hreg[h] = bload16<T>(rh, hoff[h]);
+        }
+        __syncthreads();
+
+        const auto rd = make_rsrc(dst + (long long)zc * plane, plane_bytes);
+#pragma unroll
+        for (int o = 0; o < TY; ++o) {
+            const Vec16<T> c = Q[(phase + RZ) % NQ][o];
+            T acc[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[e] = wz[RZ] * c.e[e];
+            // z neighbours from the queue
+#pragma unroll
+            for (int i = 0; i < 2 * RZ + 1; ++i) {
+                if (i == RZ)
+                    continue;
+                const Vec16<T> v = Q[(phase + i) % NQ][o];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[e] = fma(wz[i], v.e[e], acc[e]);
+            }
+            // y neighbours: own rows from the queue, the others from LDS
+#pragma unroll
+            for (int i = 0; i < 2 * R; ++i) {
+                const int oy = i < R ? i - R : i - R + 1;
+                const int row = o + oy;
+                Vec16<T> v;
+                if (row >= 0 && row < TY)
+                    v = Q[(phase + RZ) % NQ][row];
+                else
+                    v = buf[((R + strip + row) * LDW + HX + lxi * VEC) / VEC];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[e] = fma(wy[i], v.e[e], acc[e]);
+            }
+            // x neighbours from the LDS row: HX elements each side
+            T xs[2 * HX + VEC];
+            const int rowbase = ((R + strip + o) * LDW + lxi * VEC) / VEC;
+#pragma unroll
+            for (int k = 0; k < HX / VEC; ++k) {
+                const Vec16<T> l = buf[rowbase + k];
+                const Vec16<T> r = buf[rowbase + (HX + VEC) / VEC + k];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    xs[k * VEC + e] = l.e[e];
+                    xs[HX + VEC + k * VEC + e] = r.e[e];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                xs[HX + e] = c.e[e];
+#pragma unroll
+            for (int i = 0; i < 2 * R; ++i) {
+                const int ox = i < R ? i - R : i - R + 1;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[e] = fma(wx[i], xs[HX + e + ox], acc[e]);
+            }
+            Vec16<T> res;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                res.e[e] = acc[e];
+            bstore16<T>(rd, sto[o], res);
+        }
+        // the slot of queue position 0 is free: prefetch plane zc + dir * (R + 2)
+        if (ZAXIS && m + R + 2 <= n - 1 + R) {
+            const auto rq = plane_rsrc(zc + dir * (R + 2));
+#pragma unroll
+            for (int o = 0; o < TY; ++o)
+                Q[phase][o] = bload16<T>(rq, own[o]);
+        }
+    };
+
+    if (!ZAXIS) {
+        step(0, 0);
+        return;
+    }
+    for (int m0 = 0; m0 < n; m0 += NQ) {
+#pragma unroll
+        for (int ph = 0; ph < NQ; ++ph) {
+            if (m0 + ph >= n)
+                break;
+            step(m0 + ph, ph);
+        }
+    }
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *s = std::getenv(name);
+    return (s && *s) ? std::atoi(s) : dflt;
+}
+
+template <typename T, int R, int TY, bool ZAXIS>
+StarParams make_params(const Geometry &g)
+{
+    using S = StarShape<T, R, TY, ZAXIS>;
+    StarParams p{};
+    p.nz = int(g.nz);
+    p.ny = int(g.ny);
+    p.nx = int(g.nx);
+    p.vol = g.vol;
+    p.ntx = int((g.nx + S::TXW - 1) / S::TXW);
+    p.nty = int((g.ny + S::TYW - 1) / S::TYW);
+    p.channels = g.channels;
+    const long long base = g.batch * p.ntx * p.nty;
+    long long nzc = 1;
+    if (ZAXIS) {
+        // enough workgroups for 256 CUs, with chunks of at least 4 queue depths
+        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 1024);
+        nzc = (target + base - 1) / base;
+        const long long min_len = 4 * (2 * R + 1);
+        const long long max_chunks = (p.nz + min_len - 1) / min_len;
+        if (nzc > max_chunks)
+            nzc = max_chunks;
+        if (nzc < 1)
+            nzc = 1;
+    }
+    p.zc = int((p.nz + nzc - 1) / nzc);
+    const int zc_env = env_int("STENCIL_STAR_ZC", 0);
+    if (ZAXIS && zc_env > 0)
+        p.zc = zc_env < p.nz ? zc_env : p.nz;
+    p.nzc = (p.nz + p.zc - 1) / p.zc;
+    p.nblocks = int(base * p.nzc);
+    return p;
+}
+
+template <typename T, int R, int TY, bool ZAXIS>
+hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    const StarParams p = make_params<T, R, TY, ZAXIS>(g);
+    const T *s = static_cast<const T *>(src);
+    T *d = static_cast<T *>(dst);
+    const T *wt = static_cast<const T *>(w);
+    if (g.boundary == STENCIL_PERIODIC)
+        stencil_star_stream_kernel<T, R, TY, true, ZAXIS>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    else
+        stencil_star_stream_kernel<T, R, TY, false, ZAXIS>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    return hipGetLastError();
+}
+
+template <typename T, bool ZAXIS>
+hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    switch (g.radius) {
+    case 1: return launch_r<T, 1, 2, ZAXIS>(g, src, dst, w, stream);
+    case 2: return launch_r<T, 2, 2, ZAXIS>(g, src, dst, w, stream);
+    case 3: return launch_r<T, 3, 2, ZAXIS>(g, src, dst, w, stream);
+    case 4: return launch_r<T, 4, 2, ZAXIS>(g, src, dst, w, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool star_stream_supported(const Geometry &g)
+{
+    if (g.shape != STENCIL_STAR || g.radius < 1 || g.radius > 4 || g.field)
+        return false;
+    const int vec = (g.dtype == STENCIL_F32) ? 4 : 2;
+    if (g.nx % vec != 0)
+        return false;
+    // byte offsets within a plane stay below the out-of-range marker; blocks fit int
+    return g.ny * g.nx * int64_t(g.elt) < (int64_t(1) << 30) &&
+           g.batch * g.ny * g.nx < (int64_t(1) << 31);
+}
+
+hipError_t launch_star_stream(const Geometry &g, const void *src, void *dst, const void *w,
+                              hipStream_t stream)
+{
+    const bool z = g.ndim == 3;
+    if (g.dtype == STENCIL_F32)
+        return z ? launch_t<float, true>(g, src, dst, w, stream)
+                 : launch_t<float, false>(g, src, dst, w, stream);
+    return z ? launch_t<double, true>(g, src, dst, w, stream)
+             : launch_t<double, false>(g, src, dst, w, stream);
+}
+
+}  // namespace stencil

@@ -49,6 +49,15 @@ struct Plan {
 hipError_t launch_generic(const Geometry &g, const void *src, void *dst, const void *field,
                           const void *w, hipStream_t stream);
 
+// Kernel families behind the streaming variant.
+bool box_stream_supported(const Geometry &g);
+hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, const void *field,
+                             const void *w, hipStream_t stream);
+
+bool star_stream_supported(const Geometry &g);
+hipError_t launch_star_stream(const Geometry &g, const void *src, void *dst, const void *w,
+                              hipStream_t stream);
+
 // 2.5D z-streaming kernels.  `supported` says whether the kernel family can run a
 // geometry (shape, radius, alignment of the x extent); launch_* run one pass.
 bool stream_supported(const Geometry &g);

@@ -89,9 +89,11 @@ def test_plan_rejects_bad_ndim_and_null():
     assert B.load().stencil_plan(ctypes.byref(desc3()), None) == B.ERR_INVALID_ARG
 
 
-def test_forced_stream_variant_needs_3d():
-    d2 = B.make_desc(2, (64, 64), variant=B.VARIANT_STREAM)
-    assert status_of(B.stencil_plan, d2) == B.ERR_UNSUPPORTED
+def test_forced_stream_variant_rejects_what_it_cannot_tile():
+    for d in (B.make_desc(2, (64, 64), shape=B.BOX, radius=3, variant=B.VARIANT_STREAM),
+              B.make_desc(3, (8, 8, 10), shape=B.STAR, variant=B.VARIANT_STREAM),  # x % 4
+              B.make_desc(3, (8, 8, 8), shape=B.BOX, radius=2, variant=B.VARIANT_STREAM)):
+        assert status_of(B.stencil_plan, d) == B.ERR_UNSUPPORTED
 
 
 def test_plan_and_query_without_gpu():
