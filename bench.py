@@ -38,6 +38,27 @@ KERNEL_SOURCES = {
 }
 
 
+DATA = {
+    "laplace2d": "i.i.d. U[-1,1] input",
+    "star7": "i.i.d. U[-1,1] input",
+    "fd8": "8 random-phase sinusoids + 1% uniform noise",
+    "box_field": "i.i.d. U[-1,1] input, 27 U[-1,1] weights with sum|w|=1, field U[0.5,1]",
+    "conv": "i.i.d. N(0,1) input, per-channel U[-1,1] weights with sum|w|=1",
+    "box_uniform": "i.i.d. U[-1,1] input, U[-1,1] weights with sum|w|=1",
+}
+
+
+def describe(wl) -> str:
+    shape = "star" if wl.shape == 0 else "box"
+    pts = wl.npoints
+    bnd = "zero" if wl.boundary == 0 else "periodic"
+    dims = "x".join(str(d) for d in wl.dims)
+    batch = " x %d volumes (N=%d, C=%d)" % (wl.batch, wl.n, wl.channels) if wl.batch > 1 else ""
+    field = " with coefficient field" if wl.has_field else ""
+    return "%dD %d-point %s R=%d%s, %s%s %s, %s boundary, %d steps per call" % (
+        wl.ndim, pts, shape, wl.radius, field, dims, batch, wl.dtype, bnd, wl.steps)
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -193,6 +214,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true", help="headline workload only")
     ap.add_argument("--cpu-planes", type=int, default=24)
+    ap.add_argument("--copy-only", action="store_true",
+                    help="run only the copy probe (counter calibration runs)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -210,6 +233,10 @@ def main() -> int:
         return 1
     B.load()
     stream = torch.cuda.Stream()
+    if args.copy_only:
+        probe = copy_probe(torch, stream, reps=args.steps)
+        print(json.dumps({"copy_probe": probe}), flush=True)
+        return 0
     wl = inputs.WORKLOADS[args.workload]
 
     head = Runner(torch, B, inputs, wl, stream)
@@ -265,10 +292,9 @@ def main() -> int:
         "metric": "stencil Gpoints/s and achieved HBM GB/s (% of MI355X peak), 3D fp32 512^3",
         "value": fig["gpoints_per_s"], "unit": "Gpoints/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic (seeded: 8 random-phase sinusoids + 1% uniform noise)",
-        "config": {"workload": "3D 25-point star R=4 (8th-order Laplacian, sum|w|=1), "
-                               "512^3 fp32, zero boundary, 4 steps per call",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic, seeded: " + DATA[wl.recipe],
+        "config": {"workload": describe(wl),
                    "dims": list(wl.dims), "stencil_steps_per_call": wl.steps,
                    "kernel": head.kernel, "variant": head.variant,
                    "temporal_depth": head.depth, "parallelism": "single GPU"},

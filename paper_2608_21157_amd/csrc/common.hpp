@@ -73,6 +73,9 @@ __device__ __forceinline__ T from_right_lane(T v, T old)
 // zero and a store there is dropped, which is how out-of-grid rows read the zero padding.
 constexpr int kBufferWord3 = 0x00020000;
 constexpr int kOutOfRange = 0x7FFFFFF0;  // an offset beyond every resource built here
+// cache policy of a buffer access: 0 = default, kNonTemporal = streamed past the caches
+// (data read or written once); it measurably raises read+write HBM throughput
+constexpr int kNonTemporal = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes)
 {
@@ -80,10 +83,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, un
                                              kBufferWord3);
 }
 
-template <typename T>
+template <typename T, int CP = 0>
 __device__ __forceinline__ Vec16<T> bload16(__amdgpu_buffer_rsrc_t r, int off)
 {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CP);
     Vec16<T> out;
     __builtin_memcpy(&out, &v, 16);
     return out;
@@ -102,12 +105,12 @@ __device__ __forceinline__ double bload1(__amdgpu_buffer_rsrc_t r, int off, doub
     return d;
 }
 
-template <typename T>
+template <typename T, int CP = 0>
 __device__ __forceinline__ void bstore16(__amdgpu_buffer_rsrc_t r, int off, const Vec16<T> &v)
 {
     __attribute__((ext_vector_type(4))) unsigned int u;
     __builtin_memcpy(&u, &v, 16);
-    __builtin_amdgcn_raw_buffer_store_b128(u, r, off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(u, r, off, 0, CP);
 }
 
 __device__ __forceinline__ int wrap_index(int q, int n)

@@ -51,7 +51,7 @@ __device__ __forceinline__ T madd(T a, T b, T c)
     return fma(a, b, c);
 }
 
-template <typename T, int TY, bool PERIODIC, bool FIELD>
+template <typename T, int TY, bool PERIODIC, bool FIELD, int STORE_CP>
 __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ field,
     const T *__restrict__ w, BoxParams p)
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
             const auto rk = make_rsrc(kf + (long long)(z0 + q) * plane, plane_bytes);
 #pragma unroll
             for (int o = 0; o < TY; ++o)
-                kv[o] = bload16<T>(rk, ((y0 + o) * p.nx + x) * E);
+                kv[o] = bload16<T, kNonTemporal>(rk, ((y0 + o) * p.nx + x) * E);
         }
     };
 
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
             for (int e = 0; e < VEC; ++e)
                 v.e[e] = FIELD ? acc[s][o][e] * kv[o].e[e] : acc[s][o][e];
             const int yo = y0 + o;
-            bstore16<T>(rd, yo < p.ny ? (yo * p.nx + x) * E : kOutOfRange, v);
+            bstore16<T, STORE_CP>(rd, yo < p.ny ? (yo * p.nx + x) * E : kOutOfRange, v);
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
                 acc[s][o][e] = T(0);
@@ -276,7 +276,7 @@ BoxParams make_params(const Geometry &g)
     p.channels = g.channels;
     const long long base = g.batch * p.segs * p.ygroups;
     // enough workgroups to fill 256 CUs several times over; at least 8 planes per chunk
-    const long long target = env_int("STENCIL_BOX_TARGET_BLOCKS", 1024);
+    const long long target = env_int("STENCIL_BOX_TARGET_BLOCKS", 2048);
     long long nzc = (target + base - 1) / base;
     const long long max_chunks = (p.nz + 7) / 8;
     if (nzc > max_chunks)
@@ -292,8 +292,8 @@ BoxParams make_params(const Geometry &g)
     return p;
 }
 
-template <typename T, int TY>
-hipError_t launch_ty(const Geometry &g, const void *src, void *dst, const void *field,
+template <typename T, int TY, int CP>
+hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *field,
                      const void *w, hipStream_t stream)
 {
     const BoxParams p = make_params<T, TY>(g);
@@ -304,14 +304,23 @@ hipError_t launch_ty(const Geometry &g, const void *src, void *dst, const void *
     const dim3 grid(p.nblocks), block(256);
     const bool per = g.boundary == STENCIL_PERIODIC;
     if (per && g.field)
-        stencil_box3_stream_kernel<T, TY, true, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, true, true, CP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else if (per)
-        stencil_box3_stream_kernel<T, TY, true, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, true, false, CP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else if (g.field)
-        stencil_box3_stream_kernel<T, TY, false, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, false, true, CP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else
-        stencil_box3_stream_kernel<T, TY, false, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, false, false, CP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     return hipGetLastError();
+}
+
+template <typename T, int TY>
+hipError_t launch_ty(const Geometry &g, const void *src, void *dst, const void *field,
+                     const void *w, hipStream_t stream)
+{
+    if (streaming_stores(g))
+        return launch_cp<T, TY, kNonTemporal>(g, src, dst, field, w, stream);
+    return launch_cp<T, TY, 0>(g, src, dst, field, w, stream);
 }
 
 }  // namespace
@@ -331,7 +340,10 @@ bool box_stream_supported(const Geometry &g)
 hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, const void *field,
                              const void *w, hipStream_t stream)
 {
-    const int ty = env_int("STENCIL_BOX_TY", 8);
+    // measured on MI355X: 4-row blocks when a wavefront spans 64 lanes of one row,
+    // 8-row blocks when it spans several narrower rows
+    const int vec = (g.dtype == STENCIL_F32) ? 4 : 2;
+    const int ty = env_int("STENCIL_BOX_TY", lanes_per_row(g, vec) == 64 ? 4 : 8);
     if (g.dtype == STENCIL_F32)
         return ty == 4 ? launch_ty<float, 4>(g, src, dst, field, w, stream)
                        : launch_ty<float, 8>(g, src, dst, field, w, stream);

@@ -57,7 +57,7 @@ struct StarShape {
     static constexpr int NH = (HTB + HLR + 255) / 256;      // halo vectors per thread
 };
 
-template <typename T, int R, int TY, bool PERIODIC, bool ZAXIS>
+template <typename T, int R, int TY, bool PERIODIC, bool ZAXIS, int STORE_CP>
 __global__ __launch_bounds__(256) void stencil_star_stream_kernel(
     const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, StarParams p)
 {
@@ -266,7 +266,7 @@ __global__ __launch_bounds__(256) void stencil_star_stream_kernel(
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
                 res.e[e] = acc[e];
-            bstore16<T>(rd, sto[o], res);
+            bstore16<T, STORE_CP>(rd, sto[o], res);
         }
         // the slot of queue position 0 is free: prefetch plane zc + dir * (R + 2)
         if (ZAXIS && m + R + 2 <= n - 1 + R) {
@@ -313,7 +313,7 @@ StarParams make_params(const Geometry &g)
     long long nzc = 1;
     if (ZAXIS) {
         // enough workgroups for 256 CUs, with chunks of at least 4 queue depths
-        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 1024);
+        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 512);
         nzc = (target + base - 1) / base;
         const long long min_len = 4 * (2 * R + 1);
         const long long max_chunks = (p.nz + min_len - 1) / min_len;
@@ -331,21 +331,30 @@ StarParams make_params(const Geometry &g)
     return p;
 }
 
-template <typename T, int R, int TY, bool ZAXIS>
-hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
-                    hipStream_t stream)
+template <typename T, int R, int TY, bool ZAXIS, int CP>
+hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
+                     hipStream_t stream)
 {
     const StarParams p = make_params<T, R, TY, ZAXIS>(g);
     const T *s = static_cast<const T *>(src);
     T *d = static_cast<T *>(dst);
     const T *wt = static_cast<const T *>(w);
     if (g.boundary == STENCIL_PERIODIC)
-        stencil_star_stream_kernel<T, R, TY, true, ZAXIS>
+        stencil_star_stream_kernel<T, R, TY, true, ZAXIS, CP>
             <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
     else
-        stencil_star_stream_kernel<T, R, TY, false, ZAXIS>
+        stencil_star_stream_kernel<T, R, TY, false, ZAXIS, CP>
             <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
     return hipGetLastError();
+}
+
+template <typename T, int R, int TY, bool ZAXIS>
+hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    if (streaming_stores(g))
+        return launch_cp<T, R, TY, ZAXIS, kNonTemporal>(g, src, dst, w, stream);
+    return launch_cp<T, R, TY, ZAXIS, 0>(g, src, dst, w, stream);
 }
 
 template <typename T, bool ZAXIS>

@@ -44,6 +44,16 @@ struct Plan {
     size_t scratch_bytes = 0;
 };
 
+// Whether output stores should bypass the caches.  Streaming (non-temporal) stores raise
+// read+write HBM throughput, but a working set that fits the 256 MB Infinity Cache (in,
+// out and the ping-pong grid of a multi-step call) is better kept there.
+inline bool streaming_stores(const Geometry &g)
+{
+    const double grid = double(g.batch) * double(g.vol) * double(g.elt);
+    const double footprint = grid * (g.field ? 4.0 : 3.0);
+    return footprint > 192.0 * 1024 * 1024;
+}
+
 // Launch one pass of `depth` steps (depth <= plan.depth) from src to dst.  `w` is the
 // device weight buffer (channels * npts of the plan's dtype).
 hipError_t launch_generic(const Geometry &g, const void *src, void *dst, const void *field,
