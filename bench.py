@@ -34,6 +34,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
     "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp"],
     "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp"],
+    "stencil_star_tb2_kernel": ["kernel_star_tb.hip", "common.hpp"],
     "stencil_generic_kernel": ["kernel_generic.hip"],
 }
 
@@ -91,7 +92,7 @@ def counter_traffic(kernel: str, workload: str, algo_bytes: float):
 
 
 class Runner:
-    def __init__(self, torch, B, inputs, wl, stream):
+    def __init__(self, torch, B, inputs, wl, stream, depth=0):
         self.torch, self.B, self.wl, self.stream = torch, B, wl, stream
         import numpy as np
         t0 = time.perf_counter()
@@ -106,7 +107,7 @@ class Runner:
         desc = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
                            dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
                            radius=wl.radius, boundary=wl.boundary,
-                           has_coeff_field=self.k is not None)
+                           has_coeff_field=self.k is not None, temporal_depth=depth)
         self.plan = B.Plan(desc)
         info = self.plan.info()
         self.kernel = info.kernel.decode()
@@ -213,7 +214,10 @@ def main() -> int:
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true", help="headline workload only")
-    ap.add_argument("--cpu-planes", type=int, default=24)
+    ap.add_argument("--cpu-planes", type=int, default=320,
+                    help="z planes of the headline input the CPU oracle runs on (~10-20 s)")
+    ap.add_argument("--depth", type=int, default=0,
+                    help="stencil steps fused per launch (0: the planner's choice)")
     ap.add_argument("--copy-only", action="store_true",
                     help="run only the copy probe (counter calibration runs)")
     args = ap.parse_args()
@@ -239,7 +243,7 @@ def main() -> int:
         return 0
     wl = inputs.WORKLOADS[args.workload]
 
-    head = Runner(torch, B, inputs, wl, stream)
+    head = Runner(torch, B, inputs, wl, stream, depth=args.depth)
     ms_total = head.timed(args.steps, args.warmup)
     ms = ms_total / args.steps
     fig = figures(wl, ms)

@@ -168,7 +168,8 @@ stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan)
                     "the streaming kernels need a 3D grid with a supported shape and radius "
                     "and an x extent they can tile");
     const int max_depth = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_max_depth(g) : 1;
-    int depth = desc->temporal_depth == 0 ? max_depth : desc->temporal_depth;
+    const int dflt = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_default_depth(g) : 1;
+    int depth = desc->temporal_depth == 0 ? dflt : desc->temporal_depth;
     if (depth > max_depth)
         return fail(STENCIL_ERR_UNSUPPORTED, "temporal_depth %d exceeds %d for this variant",
                     desc->temporal_depth, max_depth);
@@ -180,7 +181,7 @@ stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan)
     p->geo = g;
     p->variant = variant;
     p->depth = depth;
-    p->kernel = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_kernel_name(g)
+    p->kernel = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_kernel_name(g, depth)
                                                     : "stencil_generic_kernel";
     p->scratch_bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
     *out_plan = reinterpret_cast<stencil_plan_t>(p);

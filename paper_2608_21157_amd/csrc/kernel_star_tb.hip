@@ -1,0 +1,424 @@
+// kernel_star_tb.hip -- two star-stencil steps fused in one pass (temporal blocking),
+// 3D, radius R <= 4, gfx950.
+//
+// Computes u2 = S(S(u0)) for the star operator S (centre plus -R..-1, +1..+R along z, y
+// and x; cross-correlation as in the HIERA "Case-study protocol", generalised to stars,
+// periodic wrap and batched volumes), reading u0 and writing u2 once, so a step costs
+// half the HBM traffic of a one-step sweep.  Under the zero boundary the intermediate
+// u1 is zero outside the grid, exactly as if it had been written and re-read.
+//
+// A workgroup owns a TXV-vector x TYW-row tile of the x-y plane and streams a chunk of
+// z planes.  Two stages run in the same loop:
+//   stage 1 computes u1 on the tile plus its R-row bands above and below and its
+//           whole-vector bands left and right (the points stage 2 reads; the corner
+//           blocks, which a star never reads, are skipped);
+//   stage 2 computes u2 on the tile, R planes behind stage 1.
+// One thread owns one column of the stage-1 region (a 16-byte vector along x): its u0
+// z-queue (2R + 1 planes plus one prefetched) and its u1 z-queue (2R + 1 planes) live in
+// registers.  Both queues rotate through the same 2R + 2 slots, so the loop is unrolled
+// 2R + 2 times and every register index is static.  The current u0 plane (stage 1's
+// in-plane neighbours, over the stage-1 region and one more band) and the current u1
+// plane (stage 2's in-plane neighbours) are staged in double-buffered LDS, one barrier
+// per plane.  Band threads use their u1 queue as the R-plane delay line that feeds the
+// u1 plane stage 2 reads.
+#include "common.hpp"
+#include "plan.hpp"
+
+#include <cstdlib>
+
+namespace stencil {
+namespace {
+
+struct Tb2Params {
+    int nz, ny, nx;
+    long long vol;
+    int ntx, nty;
+    int zc, nzc;
+    int nblocks;
+    int channels;
+};
+
+template <typename T, int R>
+struct Tb2Shape {
+    static constexpr int VEC = Vec16<T>::N;
+    static constexpr int TXV = 16;                       // tile width in vectors
+    static constexpr int TYW = 32;                       // tile height in rows
+    static constexpr int HXV = (R + VEC - 1) / VEC;      // x reach in vectors
+    static constexpr int NTILE = TXV * TYW;
+    // stage-1 bands around the tile: R rows above and below, HXV vectors left and right
+    static constexpr int NBAND_TB = 2 * R * TXV;
+    static constexpr int NBAND_LR = 2 * TYW * HXV;
+    static constexpr int NS1 = NTILE + NBAND_TB + NBAND_LR;       // stage-1 columns
+    static constexpr int THREADS = ((NS1 + 63) / 64) * 64;
+    // u0 cells stage 1 reads beyond its own columns
+    static constexpr int NX_TB = 2 * R * TXV;            // rows -2R..-R-1, TYW+R..TYW+2R-1
+    static constexpr int NX_CORNER = 2 * R * 2 * HXV;    // x reach of the top/bottom bands
+    static constexpr int NX_LR = 2 * TYW * HXV;          // x reach of the left/right bands
+    static constexpr int NEXTRA = NX_TB + NX_CORNER + NX_LR;
+    static constexpr int NEX = (NEXTRA + THREADS - 1) / THREADS;
+    // LDS rectangles: u0 over rows -2R..TYW+2R-1, vectors -2HXV..TXV+2HXV-1;
+    // u1 over rows -R..TYW+R-1, vectors -HXV..TXV+HXV-1
+    static constexpr int W0 = TXV + 4 * HXV, H0 = TYW + 4 * R;
+    static constexpr int W1 = TXV + 2 * HXV, H1 = TYW + 2 * R;
+    static constexpr int NQ = 2 * R + 2;                 // queue slots (both queues)
+};
+
+// LDS vector index of tile-relative (row r, vector v) in a rectangle whose origin is
+// (-oy, -ov) and pitch is w.
+__device__ __forceinline__ int rect_index(int r, int v, int oy, int ov, int w)
+{
+    return (r + oy) * w + (v + ov);
+}
+
+template <typename T, int R, bool PERIODIC, int STORE_CP>
+__global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_kernel(
+    const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, Tb2Params p)
+{
+    using S = Tb2Shape<T, R>;
+    constexpr int VEC = S::VEC, TXV = S::TXV, TYW = S::TYW, HXV = S::HXV, NQ = S::NQ;
+    constexpr int E = sizeof(T);
+    __shared__ Vec16<T> lds0[2][S::H0 * S::W0];
+    __shared__ Vec16<T> lds1[2][S::H1 * S::W1];
+
+    const int tid = threadIdx.x;
+    int t = xcd_logical_block(blockIdx.x, p.nblocks);
+    const int tx = t % p.ntx;
+    t /= p.ntx;
+    const int ty = t % p.nty;
+    t /= p.nty;
+    const int zi = t % p.nzc;
+    const long long b = t / p.nzc;
+    const int x0 = tx * TXV * VEC, y0 = ty * TYW;
+    const long long plane = (long long)p.ny * p.nx;
+    const unsigned plane_bytes = unsigned(plane * E);
+    const T *src = in + b * p.vol;
+    T *dst = out + b * p.vol;
+
+    // ---- this thread's stage-1 column (tile-relative row r, vector v) ------------------
+    bool col = tid < S::NS1, tile = tid < S::NTILE;
+    int r = 0, v = 0;
+    if (tile) {
+        r = tid / TXV;
+        v = tid % TXV;
+    } else if (col) {
+        int j = tid - S::NTILE;
+        if (j < S::NBAND_TB) {
+            const int k = j / TXV;
+            r = k < R ? k - R : TYW + k - R;
+            v = j % TXV;
+        } else {
+            j -= S::NBAND_TB;
+            const int k = j % (2 * HXV);
+            r = j / (2 * HXV);
+            v = k < HXV ? k - HXV : TXV + k - HXV;
+        }
+    }
+    const int gy = y0 + r, gx = x0 + v * VEC;
+    const bool inside = gy >= 0 && gy < p.ny && gx >= 0 && gx < p.nx;
+    auto goff = [&](int yy, int xx) {
+        if (PERIODIC)
+            return (wrap_index(yy, p.ny) * p.nx + wrap_index(xx, p.nx)) * E;
+        return (yy >= 0 && yy < p.ny && xx >= 0 && xx < p.nx) ? (yy * p.nx + xx) * E
+                                                               : kOutOfRange;
+    };
+    const int qoff = col ? goff(gy, gx) : kOutOfRange;
+    const int soff = (tile && inside) ? (gy * p.nx + gx) * E : kOutOfRange;
+    const int i0 = rect_index(r, v, 2 * R, 2 * HXV, S::W0);   // own cell in the u0 plane
+    const int i1 = rect_index(r, v, R, HXV, S::W1);           // own cell in the u1 plane
+
+    // ---- u0 cells beyond the stage-1 columns that this thread stages ------------------
+    int xoff[S::NEX], xidx[S::NEX];
+#pragma unroll
+    for (int h = 0; h < S::NEX; ++h) {
+        int j = tid + h * S::THREADS;
+        int rr = 0, vv = 0;
+        xidx[h] = -1;
+        xoff[h] = kOutOfRange;
+        if (j < S::NX_TB) {
+            const int k = j / TXV;
+            rr = k < R ? k - 2 * R : TYW + R + k - R;
+            vv = j % TXV;
+            xidx[h] = 0;
+        } else if ((j -= S::NX_TB) < S::NX_CORNER) {
+            const int k = j % (2 * HXV);
+            const int q = j / (2 * HXV);
+            rr = q < R ? q - R : TYW + q - R;
+            vv = k < HXV ? k - HXV : TXV + k - HXV;
+            xidx[h] = 0;
+        } else if ((j -= S::NX_CORNER) < S::NX_LR) {
+            const int k = j % (2 * HXV);
+            rr = j / (2 * HXV);
+            vv = k < HXV ? k - 2 * HXV : TXV + HXV + k - HXV;
+            xidx[h] = 0;
+        }
+        if (xidx[h] == 0) {
+            xidx[h] = rect_index(rr, vv, 2 * R, 2 * HXV, S::W0);
+            xoff[h] = goff(y0 + rr, x0 + vv * VEC);
+        }
+    }
+
+    // ---- weights: z by queue position (direction-aware), y and x by offset -------------
+    const T *wb = w + (b % p.channels) * (1 + 6 * R);
+    const int dir = (zi & 1) ? -1 : 1;
+    T wz[2 * R + 1], wy[2 * R], wx[2 * R];
+    wz[R] = wb[0];
+#pragma unroll
+    for (int i = 0; i < 2 * R; ++i) {
+        const int oz = i < R ? i - R : i - R + 1;
+        const int pos = R + dir * oz;
+#pragma unroll
+        for (int q = 0; q < 2 * R + 1; ++q)
+            if (q == pos)
+                wz[q] = wb[1 + i];
+        wy[i] = wb[1 + 2 * R + i];
+        wx[i] = wb[1 + 4 * R + i];
+    }
+
+    // ---- z range: stage 2 writes [z0, z0 + n); stage 1 runs R planes ahead -----------
+    const int z0 = zi * p.zc;
+    const int n = min(p.zc, p.nz - z0);
+    const int zs1 = dir > 0 ? z0 - R : z0 + n - 1 + R;  // stage-1 plane of iteration 0
+    const int iters = n + 2 * R;
+
+    auto plane_rsrc = [&](int z) {
+        bool ok = z >= 0 && z < p.nz;
+        if (PERIODIC) {
+            z = wrap_index(z, p.nz);
+            ok = true;
+        }
+        return make_rsrc(src + (ok ? z : 0) * plane, ok ? plane_bytes : 0u);
+    };
+    auto z_inside = [&](int z) { return PERIODIC || (z >= 0 && z < p.nz); };
+
+    // ---- queues: position i of iteration m (phase m mod NQ) is slot (phase + i) mod NQ
+    // q0 position i holds u0 at plane z1 + dir * (i - R), i = 0 .. 2R + 1 (prefetch)
+    // q1 position i holds u1 at plane z2 + dir * (i - R), i = 0 .. 2R, z2 = z1 - dir * R
+    Vec16<T> q0[NQ], q1[NQ], xr[S::NEX];
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) {
+        q0[i] = bload16<T>(plane_rsrc(zs1 + dir * (i - R)), qoff);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            q1[i].e[e] = T(0);
+    }
+    {
+        const auto rx = plane_rsrc(zs1);
+#pragma unroll
+        for (int h = 0; h < S::NEX; ++h)
+            xr[h] = bload16<T>(rx, xoff[h]);
+    }
+
+    // In-plane operands of one column: the 2R vectors above and below it and the HXV
+    // vectors left and right of it, read from LDS together before any arithmetic so
+    // that the reads are in flight at the same time.
+    constexpr int NG = 2 * R + 2 * HXV;
+    auto gather = [&](const Vec16<T> *buf, int idx, int pitch, Vec16<T> (&g)[NG]) {
+#pragma unroll
+        for (int i = 0; i < 2 * R; ++i) {
+            const int oy = i < R ? i - R : i - R + 1;
+            g[i] = buf[idx + oy * pitch];
+        }
+#pragma unroll
+        for (int k = 0; k < HXV; ++k) {
+            g[2 * R + k] = buf[idx - HXV + k];
+            g[2 * R + HXV + k] = buf[idx + 1 + k];
+        }
+    };
+    auto stencil_at = [&](const Vec16<T> (&g)[NG], const Vec16<T> (&q)[NQ], int phase) {
+        // z from the queue, y and x from the gathered in-plane operands
+        T acc[VEC];
+        const Vec16<T> c = q[(phase + R) % NQ];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[e] = wz[R] * c.e[e];
+#pragma unroll
+        for (int i = 0; i < 2 * R + 1; ++i) {
+            if (i == R)
+                continue;
+            const Vec16<T> u = q[(phase + i) % NQ];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[e] = fma(wz[i], u.e[e], acc[e]);
+        }
+#pragma unroll
+        for (int i = 0; i < 2 * R; ++i) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[e] = fma(wy[i], g[i].e[e], acc[e]);
+        }
+        T xs[(2 * HXV + 1) * VEC];
+#pragma unroll
+        for (int k = 0; k < HXV; ++k) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                xs[k * VEC + e] = g[2 * R + k].e[e];
+                xs[(HXV + 1 + k) * VEC + e] = g[2 * R + HXV + k].e[e];
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            xs[HXV * VEC + e] = c.e[e];
+#pragma unroll
+        for (int i = 0; i < 2 * R; ++i) {
+            const int ox = i < R ? i - R : i - R + 1;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[e] = fma(wx[i], xs[HXV * VEC + e + ox], acc[e]);
+        }
+        Vec16<T> res;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            res.e[e] = acc[e];
+        return res;
+    };
+
+    auto step = [&](int m, int phase) {
+        const int z1 = zs1 + dir * m;
+        const int z2 = z1 - dir * R;
+        Vec16<T> *b0 = lds0[phase & 1];
+        Vec16<T> *b1 = lds1[phase & 1];
+        // stage the u0 plane z1 (own columns and the extra cells) and the u1 plane z2
+        if (col) {
+            b0[i0] = q0[(phase + R) % NQ];
+            b1[i1] = q1[(phase + R) % NQ];
+        }
+#pragma unroll
+        for (int h = 0; h < S::NEX; ++h)
+            if (xidx[h] >= 0)
+                b0[xidx[h]] = xr[h];
+        if (m + 1 < iters) {
+            const auto rx = plane_rsrc(z1 + dir);
+#pragma unroll
+            for (int h = 0; h < S::NEX; ++h)
+                xr[h] = bload16<T>(rx, xoff[h]);
+        }
+        __syncthreads();
+
+        if (col) {
+            // each stage reads its LDS operands together before its arithmetic (reading
+            // both stages' operands up front was measured slower: register pressure)
+            const bool st2 = tile && m >= 2 * R;
+            Vec16<T> g[NG];
+            gather(b0, i0, S::W0, g);
+            // stage 1: u1 at plane z1; zero outside the grid under the zero boundary
+            Vec16<T> u1 = stencil_at(g, q0, phase);
+            if (!PERIODIC && !(inside && z_inside(z1))) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    u1.e[e] = T(0);
+            }
+            q1[(phase + 2 * R) % NQ] = u1;
+            // stage 2: u2 at plane z2 (tile columns, once the u1 queue is full)
+            if (st2) {
+                gather(b1, i1, S::W1, g);
+                const Vec16<T> u2 = stencil_at(g, q1, phase);
+                bstore16<T, STORE_CP>(make_rsrc(dst + (long long)z2 * plane, plane_bytes),
+                                      soff, u2);
+            }
+            // queue position 0 is free: prefetch u0 at plane z1 + dir * (R + 2)
+            if (m + 2 < iters)
+                q0[phase] = bload16<T>(plane_rsrc(z1 + dir * (R + 2)), qoff);
+        }
+    };
+
+    for (int m0 = 0; m0 < iters; m0 += NQ) {
+#pragma unroll
+        for (int ph = 0; ph < NQ; ++ph) {
+            if (m0 + ph >= iters)
+                break;
+            step(m0 + ph, ph);
+        }
+    }
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *s = std::getenv(name);
+    return (s && *s) ? std::atoi(s) : dflt;
+}
+
+template <typename T, int R>
+Tb2Params make_params(const Geometry &g)
+{
+    using S = Tb2Shape<T, R>;
+    Tb2Params p{};
+    p.nz = int(g.nz);
+    p.ny = int(g.ny);
+    p.nx = int(g.nx);
+    p.vol = g.vol;
+    p.ntx = int((g.nx + S::TXV * S::VEC - 1) / (S::TXV * S::VEC));
+    p.nty = int((g.ny + S::TYW - 1) / S::TYW);
+    p.channels = g.channels;
+    const long long base = g.batch * p.ntx * p.nty;
+    // two workgroups per CU measured best; chunks of at least 8 radii so the 2R-plane
+    // start-up of stage 2 stays small
+    const long long target = env_int("STENCIL_TB_TARGET_BLOCKS", 512);
+    long long nzc = (target + base - 1) / base;
+    const long long min_len = 8 * R;
+    const long long max_chunks = (p.nz + min_len - 1) / min_len;
+    if (nzc > max_chunks)
+        nzc = max_chunks;
+    if (nzc < 1)
+        nzc = 1;
+    p.zc = int((p.nz + nzc - 1) / nzc);
+    p.nzc = (p.nz + p.zc - 1) / p.zc;
+    p.nblocks = int(base * p.nzc);
+    return p;
+}
+
+template <typename T, int R, int CP>
+hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
+                     hipStream_t stream)
+{
+    using S = Tb2Shape<T, R>;
+    const Tb2Params p = make_params<T, R>(g);
+    const T *s = static_cast<const T *>(src);
+    T *d = static_cast<T *>(dst);
+    const T *wt = static_cast<const T *>(w);
+    if (g.boundary == STENCIL_PERIODIC)
+        stencil_star_tb2_kernel<T, R, true, CP>
+            <<<dim3(p.nblocks), dim3(S::THREADS), 0, stream>>>(s, d, wt, p);
+    else
+        stencil_star_tb2_kernel<T, R, false, CP>
+            <<<dim3(p.nblocks), dim3(S::THREADS), 0, stream>>>(s, d, wt, p);
+    return hipGetLastError();
+}
+
+template <typename T, int R>
+hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    if (streaming_stores(g))
+        return launch_cp<T, R, kNonTemporal>(g, src, dst, w, stream);
+    return launch_cp<T, R, 0>(g, src, dst, w, stream);
+}
+
+template <typename T>
+hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    switch (g.radius) {
+    case 1: return launch_r<T, 1>(g, src, dst, w, stream);
+    case 2: return launch_r<T, 2>(g, src, dst, w, stream);
+    case 3: return launch_r<T, 3>(g, src, dst, w, stream);
+    case 4: return launch_r<T, 4>(g, src, dst, w, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool star_tb2_supported(const Geometry &g)
+{
+    return g.ndim == 3 && star_stream_supported(g);
+}
+
+hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,
+                           hipStream_t stream)
+{
+    if (g.dtype == STENCIL_F32)
+        return launch_t<float>(g, src, dst, w, stream);
+    return launch_t<double>(g, src, dst, w, stream);
+}
+
+}  // namespace stencil

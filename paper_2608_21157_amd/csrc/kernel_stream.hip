@@ -10,13 +10,24 @@ bool stream_supported(const Geometry &g)
 
 int stream_max_depth(const Geometry &g)
 {
-    return 1;
+    return star_tb2_supported(g) ? 2 : 1;
 }
 
-const char *stream_kernel_name(const Geometry &g)
+int stream_default_depth(const Geometry &g)
+{
+    // Fusing two steps halves HBM traffic but costs redundant stage-1 work on the halo
+    // bands and LDS traffic that grow with the radius.  Measured on MI355X (512^3 and 256^3
+    // fp32): a clear win at radius 1, no gain at radius 4, where one step per launch is
+    // already close to the streaming-copy ceiling.
+    return (star_tb2_supported(g) && g.radius <= 2) ? 2 : 1;
+}
+
+const char *stream_kernel_name(const Geometry &g, int depth)
 {
     if (box_stream_supported(g))
         return "stencil_box3_stream_kernel";
+    if (star_tb2_supported(g) && depth == 2)
+        return "stencil_star_tb2_kernel";
     if (star_stream_supported(g))
         return "stencil_star_stream_kernel";
     return "";
@@ -25,6 +36,8 @@ const char *stream_kernel_name(const Geometry &g)
 hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const void *field,
                          const void *w, int depth, hipStream_t stream)
 {
+    if (depth == 2 && star_tb2_supported(g))
+        return launch_star_tb2(g, src, dst, w, stream);
     if (depth != 1)
         return hipErrorInvalidValue;
     if (box_stream_supported(g))

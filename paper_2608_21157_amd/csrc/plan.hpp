@@ -68,11 +68,17 @@ bool star_stream_supported(const Geometry &g);
 hipError_t launch_star_stream(const Geometry &g, const void *src, void *dst, const void *w,
                               hipStream_t stream);
 
+// Two star steps fused in one pass (3D).
+bool star_tb2_supported(const Geometry &g);
+hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,
+                           hipStream_t stream);
+
 // 2.5D z-streaming kernels.  `supported` says whether the kernel family can run a
 // geometry (shape, radius, alignment of the x extent); launch_* run one pass.
 bool stream_supported(const Geometry &g);
 int stream_max_depth(const Geometry &g);
-const char *stream_kernel_name(const Geometry &g);
+int stream_default_depth(const Geometry &g);
+const char *stream_kernel_name(const Geometry &g, int depth);
 hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const void *field,
                          const void *w, int depth, hipStream_t stream);
 

@@ -178,3 +178,41 @@ def test_variants_agree():
     for variant in (B.VARIANT_GENERIC, B.VARIANT_AUTO):
         got, info = run_library(wl, x, w, k, variant=variant)
         report("variant %s" % info, got, ref, tolerance(wl, x, k))
+
+
+STAR_CASES = [(R, dt, bnd) for R in (1, 2, 3, 4) for dt in ("f32", "f64")
+              for bnd in (B.ZERO, B.PERIODIC)]
+
+
+@pytest.mark.parametrize("R,dt,bnd", STAR_CASES,
+                         ids=["R%d-%s-%s" % (c[0], c[1], "zero" if c[2] == 0 else "per")
+                              for c in STAR_CASES])
+@pytest.mark.parametrize("depth", [1, 0], ids=["depth1", "auto"])
+def test_star_radius_dtype_boundary_depth(R, dt, bnd, depth):
+    """3D stars of every radius, fp32 and fp64, both boundaries, with steps fused two at
+    a time (auto) or one launch per step; ragged extents in every axis, 3 steps (one fused
+    pair plus a single step)."""
+    from dataclasses import replace
+    g = np.random.default_rng(100 + R)
+    dims = (23, 37, 72) if dt == "f32" else (21, 35, 40)
+    wl = replace(WORKLOADS["c3"].resized(dims, steps=3), radius=R, boundary=bnd, dtype=dt)
+    npdt = np.float32 if dt == "f32" else np.float64
+    x = g.uniform(-1, 1, dims).astype(npdt)
+    w = g.uniform(-1, 1, (1, wl.npoints))
+    w = (w / np.abs(w).sum()).astype(npdt)
+    got, info = run_library(wl, x, w, depth=depth)
+    ref = oracle_full(wl, x, w)
+    report("star R=%d %s bnd=%d %s" % (R, dt, bnd, info), got, ref, tolerance(wl, x))
+
+
+def test_fused_steps_match_single_steps():
+    """Two steps in one fused pass agree with two single-step launches (both against the
+    oracle, and with each other to rounding)."""
+    wl, (x, w, k) = _case("c3", (40, 33, 136), None, 2)
+    fused, i2 = run_library(wl, x, w, depth=2)
+    single, i1 = run_library(wl, x, w, depth=1)
+    assert i2["depth"] == 2 and i1["depth"] == 1
+    ref = oracle_full(wl, x, w)
+    report("fused", fused, ref, tolerance(wl, x))
+    report("single", single, ref, tolerance(wl, x))
+    assert np.abs(fused - single).max() <= 2 * tolerance(wl, x)
