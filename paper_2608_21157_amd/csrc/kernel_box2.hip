@@ -1,0 +1,320 @@
+// kernel_box2.hip -- 2D box stencils of radius R <= 4 ((2R+1)^2 points), y-streaming,
+// gfx950.
+//
+// This is the operator of the HIERA case study itself (Sec. "Implementation and Evaluation
+// Protocol", paragraph "Case-study protocol": a 2D box stencil of radius 3, i.e. a 7x7
+// zero-padded cross-correlation with padding 3 and stride 1, in FP64), with any radius up
+// to 4, fp32 or fp64, zero or periodic boundary and batched images with per-channel
+// weights.  One launch computes one step.
+//
+// Mapping (no LDS, no barriers):
+//   * a wavefront owns a row segment of 64 lanes x 16 bytes (or 64/lpr whole narrower
+//     rows, each streamed over its own rows) and streams down a chunk of rows;
+//   * each input row is loaded once (16 bytes per lane, prefetched 2R + 1 rows ahead) and
+//     folded into 2R + 1 rotating accumulator rows: input row y contributes to output rows
+//     y - R .. y + R, so output row y - R is complete and written after row y;
+//   * x neighbours come from the lanes up to HXV to the left and right through chained DPP
+//     wave shifts; only the first and last lane of a segment load the HXV 16-byte halo
+//     vectors beyond it;
+//   * buffer loads with 32-bit offsets: rows outside the grid read zero (zero boundary).
+#include "common.hpp"
+#include "plan.hpp"
+
+#include <cstdlib>
+
+namespace stencil {
+namespace {
+
+struct Box2Params {
+    int ny, nx;
+    long long vol;
+    int lpr, segw, segs;   // lanes per row segment, segment width, segments per row
+    int rg;                // row groups per wavefront (64 / lpr)
+    int yc, nyc;           // rows per chunk, chunks per image (per row group)
+    long long batch;
+    int channels;
+    int nblocks;
+};
+
+template <typename T, int R, bool PERIODIC, int STORE_CP>
+__global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
+    const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, Box2Params p)
+{
+    constexpr int VEC = Vec16<T>::N;
+    constexpr int E = sizeof(T);
+    constexpr int HXV = (R + VEC - 1) / VEC;   // x reach in vectors
+    constexpr int NS = 2 * R + 1;              // accumulator rows
+    constexpr int NW = 2 * R + 1;              // taps per axis
+    constexpr int NX = (2 * HXV + 1) * VEC;    // extended row length (elements)
+    constexpr int PF = NS;                     // input rows in flight per lane
+    const int lane = threadIdx.x & 63;
+    // the wavefront index is uniform by construction; saying so keeps everything derived
+    // from it (image, segment, weight pointer, buffer resources) in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    // work item of this wavefront: (image, segment, chunk); row group rg of the wave takes
+    // chunk * rg + its own index, so that narrow rows still use all 64 lanes
+    const long long tw = (long long)xcd_logical_block(blockIdx.x, p.nblocks) * 4 + wave;
+    const int units = p.segs * p.nyc;  // wavefront work items per image
+    const long long b = tw / units;
+    if (b >= p.batch)
+        return;  // whole wavefront leaves; the kernel has no barriers
+    const int t = int(tw - b * units);
+    const int seg = t % p.segs;
+    const int ch = t / p.segs;  // chunk index of the wavefront (row groups split it)
+    const int lx = lane % p.lpr, rgi = lane / p.lpr;
+    const int x = seg * p.segw + lx * VEC;
+    const int cidx = ch * p.rg + rgi;      // chunk of this row group
+    const int y0 = cidx * p.yc;
+    // output rows of this row group (0: idle); every row group of the wavefront runs the
+    // same number of iterations (p.yc + 2R) so the lane shifts always see active lanes,
+    // and stores beyond n are dropped
+    const int n = max(0, min(p.yc, p.ny - y0));
+    const T *src = in + b * p.vol;
+    T *dst = out + b * p.vol;
+    const unsigned img_bytes = unsigned(p.vol * E);
+    const auto rin = make_rsrc(src, img_bytes);
+    const auto rout = make_rsrc(dst, img_bytes);
+    const T *wb = w + (b % p.channels) * (NW * NW);
+
+    // halo vectors: the first lane of a segment holds the HXV vectors left of it, the last
+    // lane the HXV vectors right of it (a segment has at least two lanes)
+    const bool first = lx == 0, last = lx == p.lpr - 1;
+    int hx[HXV];
+    bool hok[HXV];
+#pragma unroll
+    for (int k = 0; k < HXV; ++k) {
+        int xx = first ? seg * p.segw - (k + 1) * VEC : seg * p.segw + p.segw + k * VEC;
+        bool ok = (first || last) && xx >= 0 && xx < p.nx;
+        if (PERIODIC) {
+            xx = wrap_index(xx, p.nx);
+            ok = first || last;
+        }
+        hx[k] = xx;
+        hok[k] = ok;
+    }
+    // byte offsets of row y: own vector and halo vectors (out of range: reads zero)
+    auto row_off = [&](int y, int &own, int (&ho)[HXV]) {
+        bool ok = y >= 0 && y < p.ny;
+        if (PERIODIC) {
+            y = wrap_index(y, p.ny);
+            ok = true;
+        }
+        own = ok ? (y * p.nx + x) * E : kOutOfRange;
+#pragma unroll
+        for (int k = 0; k < HXV; ++k)
+            ho[k] = (ok && hok[k]) ? (y * p.nx + hx[k]) * E : kOutOfRange;
+    };
+
+    // rolling queue of PF input rows (row k of the chunk's input is slot k mod PF)
+    Vec16<T> qv[PF], qh[PF][HXV];
+    const int nin = p.yc + 2 * R;  // input rows y0 - R .. y0 + yc - 1 + R
+#pragma unroll
+    for (int s = 0; s < PF; ++s) {
+        int own, ho[HXV];
+        row_off(y0 - R + s, own, ho);
+        qv[s] = bload16<T>(rin, s < nin ? own : kOutOfRange);
+#pragma unroll
+        for (int k = 0; k < HXV; ++k)
+            qh[s][k] = bload16<T>(rin, s < nin ? ho[k] : kOutOfRange);
+    }
+
+    T acc[NS][VEC];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[s][e] = T(0);
+
+    // Fold input row k (y = y0 - R + k).  Offset (a, c) in weight order is (oy, ox) =
+    // (a - R, c - R); the input point feeds output row q = k - a (relative to y0), slot
+    // q mod NS.  Rows q outside [0, yc) are skipped (uniform across the wavefront).
+    auto fold = [&](int k, int pslot, auto slot_of_q) {
+        const Vec16<T> own = qv[pslot];
+        // extended row: vectors of lanes -HXV .. +HXV (halo at the segment's ends)
+        Vec16<T> lft[HXV], rgt[HXV];
+#pragma unroll
+        for (int j = 0; j < HXV; ++j) {
+            const Vec16<T> &sl = j == 0 ? own : lft[j - 1];
+            const Vec16<T> &sr = j == 0 ? own : rgt[j - 1];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const T l = from_left_lane(sl.e[e], qh[pslot][j].e[e]);
+                const T r = from_right_lane(sr.e[e], qh[pslot][j].e[e]);
+                lft[j].e[e] = first ? qh[pslot][j].e[e] : l;
+                rgt[j].e[e] = last ? qh[pslot][j].e[e] : r;
+            }
+        }
+        T ext[NX];
+#pragma unroll
+        for (int j = 0; j < HXV; ++j)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                ext[(HXV - 1 - j) * VEC + e] = lft[j].e[e];
+                ext[(HXV + 1 + j) * VEC + e] = rgt[j].e[e];
+            }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            ext[HXV * VEC + e] = own.e[e];
+        // refill the slot with input row k + PF
+        if (k + PF < nin) {
+            int o2, h2[HXV];
+            row_off(y0 - R + k + PF, o2, h2);
+            qv[pslot] = bload16<T>(rin, o2);
+#pragma unroll
+            for (int j = 0; j < HXV; ++j)
+                qh[pslot][j] = bload16<T>(rin, h2[j]);
+        }
+#pragma unroll
+        for (int a = 0; a < NW; ++a) {
+            const int q = k - a;
+            if (q < 0 || q >= p.yc)
+                continue;
+            const int s = slot_of_q(a);
+#pragma unroll
+            for (int c = 0; c < NW; ++c) {
+                const T wv = wb[a * NW + c];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[s][e] = fma(wv, ext[HXV * VEC + e + c - R], acc[s][e]);
+            }
+        }
+        // output row k - 2R is complete
+        const int qd = k - 2 * R;
+        if (qd >= 0 && qd < p.yc) {
+            const int sd = slot_of_q(2 * R);
+            Vec16<T> v;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                v.e[e] = acc[sd][e];
+                acc[sd][e] = T(0);
+            }
+            bstore16<T, STORE_CP>(rout, qd < n ? ((y0 + qd) * p.nx + x) * E : kOutOfRange, v);
+        }
+    };
+
+    // unrolled NS times (PF = NS) so that queue and accumulator slots are static
+    for (int k0 = 0; k0 < nin; k0 += NS) {
+#pragma unroll
+        for (int j = 0; j < NS; ++j) {
+            const int k = k0 + j;
+            if (k >= nin)
+                break;
+            fold(k, j, [j](int a) { return ((j - a) % NS + NS) % NS; });
+        }
+    }
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *s = std::getenv(name);
+    return (s && *s) ? std::atoi(s) : dflt;
+}
+
+int lanes_per_row(const Geometry &g, int vec)
+{
+    if (g.nx % vec != 0)
+        return 0;
+    const int64_t nxv = g.nx / vec;
+    if (nxv >= 64)
+        return (nxv % 64 == 0) ? 64 : 0;
+    return (nxv >= 2 && 64 % nxv == 0) ? int(nxv) : 0;
+}
+
+template <typename T, int R>
+Box2Params make_params(const Geometry &g)
+{
+    constexpr int VEC = Vec16<T>::N;
+    Box2Params p{};
+    p.ny = int(g.ny);
+    p.nx = int(g.nx);
+    p.vol = g.vol;
+    p.lpr = lanes_per_row(g, VEC);
+    p.segw = p.lpr * VEC;
+    p.segs = p.nx / p.segw;
+    p.rg = 64 / p.lpr;
+    p.batch = g.batch;
+    p.channels = g.channels;
+    // about 16 wavefronts per CU in total; chunks of at least 16 radii of rows so the
+    // 2R-row overlap between chunks stays small
+    const long long target = env_int("STENCIL_BOX2_TARGET_WAVES", 4096);
+    const long long per_image = g.batch * p.segs;
+    long long rows_units = (target + per_image - 1) / per_image;  // row groups per image
+    long long nchunks = rows_units;
+    const long long min_len = 16 * R;
+    const long long max_chunks = (p.ny + min_len - 1) / min_len;
+    if (nchunks > max_chunks)
+        nchunks = max_chunks;
+    if (nchunks < 1)
+        nchunks = 1;
+    // chunks are taken rg at a time by a wavefront
+    long long total = ((nchunks + p.rg - 1) / p.rg) * p.rg;
+    p.yc = int((p.ny + total - 1) / total);
+    p.nyc = int(((p.ny + p.yc - 1) / p.yc + p.rg - 1) / p.rg);
+    const long long waves = g.batch * p.segs * p.nyc;
+    p.nblocks = int((waves + 3) / 4);
+    return p;
+}
+
+template <typename T, int R, int CP>
+hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
+                     hipStream_t stream)
+{
+    const Box2Params p = make_params<T, R>(g);
+    const T *s = static_cast<const T *>(src);
+    T *d = static_cast<T *>(dst);
+    const T *wt = static_cast<const T *>(w);
+    if (g.boundary == STENCIL_PERIODIC)
+        stencil_box2_stream_kernel<T, R, true, CP>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    else
+        stencil_box2_stream_kernel<T, R, false, CP>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    return hipGetLastError();
+}
+
+template <typename T, int R>
+hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    if (streaming_stores(g))
+        return launch_cp<T, R, kNonTemporal>(g, src, dst, w, stream);
+    return launch_cp<T, R, 0>(g, src, dst, w, stream);
+}
+
+template <typename T>
+hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *w,
+                    hipStream_t stream)
+{
+    switch (g.radius) {
+    case 1: return launch_r<T, 1>(g, src, dst, w, stream);
+    case 2: return launch_r<T, 2>(g, src, dst, w, stream);
+    case 3: return launch_r<T, 3>(g, src, dst, w, stream);
+    case 4: return launch_r<T, 4>(g, src, dst, w, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool box2_stream_supported(const Geometry &g)
+{
+    if (g.ndim != 2 || g.shape != STENCIL_BOX || g.radius < 1 || g.radius > 4 || g.field)
+        return false;
+    const int vec = (g.dtype == STENCIL_F32) ? 4 : 2;
+    if (lanes_per_row(g, vec) == 0)
+        return false;
+    // 32-bit byte offsets within one image; block count fits int
+    return g.vol * int64_t(g.elt) < (int64_t(1) << 30) &&
+           g.batch * (g.nx / vec) < (int64_t(1) << 30);
+}
+
+hipError_t launch_box2_stream(const Geometry &g, const void *src, void *dst, const void *w,
+                              hipStream_t stream)
+{
+    if (g.dtype == STENCIL_F32)
+        return launch_t<float>(g, src, dst, w, stream);
+    return launch_t<double>(g, src, dst, w, stream);
+}
+
+}  // namespace stencil

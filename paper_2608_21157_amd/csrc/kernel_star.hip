@@ -7,11 +7,11 @@
 // sets, periodic wrap and batched volumes.
 //
 // Mapping:
-//   * a workgroup (4 wavefronts) owns a TXW x TYW tile of the x-y plane and streams a
+//   * a workgroup (NW wavefronts) owns a TXW x TYW tile of the x-y plane and streams a
 //     chunk of z planes; a lane owns a 16-byte vector along x times TY rows along y;
 //   * z neighbours: every lane keeps the 2R + 1 planes around the current one for its own
-//     points in registers (a queue of 2R + 2 slots, one of them the prefetched next
-//     plane), so each input point is loaded from HBM once per chunk;
+//     points in registers (a queue of 2R + 1 + PF slots, PF of them prefetched planes),
+//     so each input point is loaded from HBM once per chunk;
 //   * x and y neighbours: the current plane is staged in LDS with an R-row halo above and
 //     below and a whole-vector halo left and right (corners are never read by a star and
 //     are not loaded); the halo is loaded one plane ahead into registers;
@@ -28,9 +28,6 @@
 namespace stencil {
 namespace {
 
-constexpr int kLanesX = 16;                  // lanes along x in a row group
-constexpr int kRowGroups = 64 / kLanesX;     // row groups per wavefront
-constexpr int kWaves = 4;
 
 struct StarParams {
     int nz, ny, nx;
@@ -41,27 +38,36 @@ struct StarParams {
     int channels;
 };
 
-template <typename T, int R, int TY, bool ZAXIS>
+template <typename T, int R, int TY, bool ZAXIS, int LX = 16, int NW = 4, int PF = 1>
 struct StarShape {
+    static constexpr int kLanesX = LX;                 // lanes along x in a row group
+    static constexpr int kRowGroups = 64 / LX;         // row groups per wavefront
+    static constexpr int kWaves = NW;                  // wavefronts per workgroup
+    static constexpr int THREADS = 64 * NW;
     static constexpr int VEC = Vec16<T>::N;
     static constexpr int TXW = kLanesX * VEC;
     static constexpr int TYW = kWaves * kRowGroups * TY;
     static constexpr int HX = ((R + VEC - 1) / VEC) * VEC;  // x halo in whole vectors
     static constexpr int LDW = TXW + 2 * HX;                // LDS row pitch (elements)
     static constexpr int LDH = TYW + 2 * R;
-    static constexpr int NQ = ZAXIS ? 2 * R + 2 : 1;        // queue slots
+    // queue slots: the 2R + 1 planes around the current one plus PF prefetched planes
+    // (PF odd, so that the slot count is even and the LDS buffer parity stays static)
+    static constexpr int NQ = ZAXIS ? 2 * R + 1 + PF : 1;
     static constexpr int NBUF = ZAXIS ? 2 : 1;
     // halo vectors per plane: R rows above and below (tile width), HX columns left/right
     static constexpr int HTB = 2 * R * (TXW / VEC);
     static constexpr int HLR = 2 * TYW * (HX / VEC);
-    static constexpr int NH = (HTB + HLR + 255) / 256;      // halo vectors per thread
+    static constexpr int NH = (HTB + HLR + THREADS - 1) / THREADS;  // halo vectors per thread
 };
 
-template <typename T, int R, int TY, bool PERIODIC, bool ZAXIS, int STORE_CP>
-__global__ __launch_bounds__(256) void stencil_star_stream_kernel(
+template <typename T, int R, int TY, bool PERIODIC, bool ZAXIS, int STORE_CP, int LX, int NW,
+          int PF>
+__global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
     const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, StarParams p)
 {
-    using S = StarShape<T, R, TY, ZAXIS>;
+    using S = StarShape<T, R, TY, ZAXIS, LX, NW, PF>;
+    static_assert(!ZAXIS || S::NQ % 2 == 0, "queue length must be even");
+    constexpr int kLanesX = S::kLanesX, kRowGroups = S::kRowGroups;
     constexpr int VEC = S::VEC, TXW = S::TXW, TYW = S::TYW, HX = S::HX, LDW = S::LDW;
     constexpr int NQ = S::NQ, NH = S::NH;
     constexpr int E = sizeof(T);
@@ -108,7 +114,7 @@ __global__ __launch_bounds__(256) void stencil_star_stream_kernel(
     int hoff[NH], hlds[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-        const int idx = tid + 256 * h;
+        const int idx = tid + S::THREADS * h;
         int ly = 0, lc = 0;
         hlds[h] = -1;
         hoff[h] = kOutOfRange;
@@ -172,7 +178,7 @@ __global__ __launch_bounds__(256) void stencil_star_stream_kernel(
 
     Vec16<T> Q[NQ][TY];
     Vec16<T> hreg[NH];
-    // prologue: queue positions 0 .. 2R + 1 hold planes zs + dir * (i - R); halo of zs
+    // prologue: queue positions 0 .. 2R + PF hold planes zs + dir * (i - R); halo of zs
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
         const auto rq = plane_rsrc(zs + dir * (i - RZ));
@@ -268,9 +274,10 @@ __global__ __launch_bounds__(256) void stencil_star_stream_kernel(
                 res.e[e] = acc[e];
             bstore16<T, STORE_CP>(rd, sto[o], res);
         }
-        // the slot of queue position 0 is free: prefetch plane zc + dir * (R + 2)
-        if (ZAXIS && m + R + 2 <= n - 1 + R) {
-            const auto rq = plane_rsrc(zc + dir * (R + 2));
+        // the slot of queue position 0 is free: prefetch plane zc + dir * (R + PF + 1),
+        // which is first used PF + 1 planes from now
+        if (ZAXIS && m + PF + 1 <= n - 1) {
+            const auto rq = plane_rsrc(zc + dir * (R + PF + 1));
 #pragma unroll
             for (int o = 0; o < TY; ++o)
                 Q[phase][o] = bload16<T>(rq, own[o]);
@@ -297,10 +304,10 @@ int env_int(const char *name, int dflt)
     return (s && *s) ? std::atoi(s) : dflt;
 }
 
-template <typename T, int R, int TY, bool ZAXIS>
+template <typename T, int R, int TY, bool ZAXIS, int LX, int NW>
 StarParams make_params(const Geometry &g)
 {
-    using S = StarShape<T, R, TY, ZAXIS>;
+    using S = StarShape<T, R, TY, ZAXIS, LX, NW>;
     StarParams p{};
     p.nz = int(g.nz);
     p.ny = int(g.ny);
@@ -313,7 +320,7 @@ StarParams make_params(const Geometry &g)
     long long nzc = 1;
     if (ZAXIS) {
         // enough workgroups for 256 CUs, with chunks of at least 4 queue depths
-        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 512);
+        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 256);
         nzc = (target + base - 1) / base;
         const long long min_len = 4 * (2 * R + 1);
         const long long max_chunks = (p.nz + min_len - 1) / min_len;
@@ -331,21 +338,33 @@ StarParams make_params(const Geometry &g)
     return p;
 }
 
-template <typename T, int R, int TY, bool ZAXIS, int CP>
-hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
-                     hipStream_t stream)
+template <typename T, int R, int TY, bool ZAXIS, int CP, int LX, int NW, int PF>
+hipError_t launch_shape(const Geometry &g, const void *src, void *dst, const void *w,
+                        hipStream_t stream)
 {
-    const StarParams p = make_params<T, R, TY, ZAXIS>(g);
+    const StarParams p = make_params<T, R, TY, ZAXIS, LX, NW>(g);
     const T *s = static_cast<const T *>(src);
     T *d = static_cast<T *>(dst);
     const T *wt = static_cast<const T *>(w);
     if (g.boundary == STENCIL_PERIODIC)
-        stencil_star_stream_kernel<T, R, TY, true, ZAXIS, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+        stencil_star_stream_kernel<T, R, TY, true, ZAXIS, CP, LX, NW, PF>
+            <<<dim3(p.nblocks), dim3(64 * NW), 0, stream>>>(s, d, wt, p);
     else
-        stencil_star_stream_kernel<T, R, TY, false, ZAXIS, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+        stencil_star_stream_kernel<T, R, TY, false, ZAXIS, CP, LX, NW, PF>
+            <<<dim3(p.nblocks), dim3(64 * NW), 0, stream>>>(s, d, wt, p);
     return hipGetLastError();
+}
+
+// Tile shape, measured on MI355X (512^3, radius 4): 64 x 64 tiles (8 wavefronts) with one
+// prefetched plane were the fastest of the 16/32/64-lane-wide, 4/8-wavefront and 1/3/5-plane
+// prefetch variants (all within a few percent); 2D grids use 64 x 32 tiles for more tiles.
+template <typename T, int R, int TY, bool ZAXIS, int CP>
+hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
+                     hipStream_t stream)
+{
+    if (ZAXIS)
+        return launch_shape<T, R, TY, ZAXIS, CP, 16, 8, 1>(g, src, dst, w, stream);
+    return launch_shape<T, R, TY, ZAXIS, CP, 16, 4, 1>(g, src, dst, w, stream);
 }
 
 template <typename T, int R, int TY, bool ZAXIS>

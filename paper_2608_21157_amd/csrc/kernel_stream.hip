@@ -5,7 +5,7 @@ namespace stencil {
 
 bool stream_supported(const Geometry &g)
 {
-    return box_stream_supported(g) || star_stream_supported(g);
+    return box_stream_supported(g) || box2_stream_supported(g) || star_stream_supported(g);
 }
 
 int stream_max_depth(const Geometry &g)
@@ -26,6 +26,8 @@ const char *stream_kernel_name(const Geometry &g, int depth)
 {
     if (box_stream_supported(g))
         return "stencil_box3_stream_kernel";
+    if (box2_stream_supported(g))
+        return "stencil_box2_stream_kernel";
     if (star_tb2_supported(g) && depth == 2)
         return "stencil_star_tb2_kernel";
     if (star_stream_supported(g))
@@ -42,6 +44,8 @@ hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const vo
         return hipErrorInvalidValue;
     if (box_stream_supported(g))
         return launch_box_stream(g, src, dst, field, w, stream);
+    if (box2_stream_supported(g))
+        return launch_box2_stream(g, src, dst, w, stream);
     if (star_stream_supported(g))
         return launch_star_stream(g, src, dst, w, stream);
     return hipErrorInvalidValue;

@@ -68,6 +68,10 @@ bool star_stream_supported(const Geometry &g);
 hipError_t launch_star_stream(const Geometry &g, const void *src, void *dst, const void *w,
                               hipStream_t stream);
 
+bool box2_stream_supported(const Geometry &g);
+hipError_t launch_box2_stream(const Geometry &g, const void *src, void *dst, const void *w,
+                              hipStream_t stream);
+
 // Two star steps fused in one pass (3D).
 bool star_tb2_supported(const Geometry &g);
 hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,

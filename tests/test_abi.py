@@ -90,17 +90,43 @@ def test_plan_rejects_bad_ndim_and_null():
 
 
 def test_forced_stream_variant_rejects_what_it_cannot_tile():
-    for d in (B.make_desc(2, (64, 64), shape=B.BOX, radius=3, variant=B.VARIANT_STREAM),
+    for d in (B.make_desc(2, (64, 66), shape=B.BOX, radius=3, variant=B.VARIANT_STREAM),  # x % 4
+              B.make_desc(2, (64, 4 * 96), shape=B.BOX, radius=3, variant=B.VARIANT_STREAM),
+              B.make_desc(2, (64, 64), shape=B.BOX, radius=3, has_coeff_field=True,
+                          variant=B.VARIANT_STREAM),
               B.make_desc(3, (8, 8, 10), shape=B.STAR, variant=B.VARIANT_STREAM),  # x % 4
               B.make_desc(3, (8, 8, 8), shape=B.BOX, radius=2, variant=B.VARIANT_STREAM)):
         assert status_of(B.stencil_plan, d) == B.ERR_UNSUPPORTED
 
 
+def test_planner_choices():
+    """The planner picks the tiled kernel family and temporal depth per description."""
+    cases = [
+        (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=4), "stencil_star_stream_kernel", 1),
+        (B.make_desc(3, (256,) * 3, shape=B.STAR, radius=1), "stencil_star_tb2_kernel", 2),
+        (B.make_desc(3, (512,) * 3, shape=B.BOX, radius=1, has_coeff_field=True,
+                     boundary=B.PERIODIC), "stencil_box3_stream_kernel", 1),
+        (B.make_desc(3, (128,) * 3, batch=256, channels=32, shape=B.BOX, radius=1),
+         "stencil_box3_stream_kernel", 1),
+        (B.make_desc(2, (10240, 10240), shape=B.BOX, radius=3, dtype=B.F64),
+         "stencil_box2_stream_kernel", 1),
+        (B.make_desc(2, (256, 256), shape=B.STAR, radius=1), "stencil_star_stream_kernel", 1),
+        (B.make_desc(3, (8, 8, 10), shape=B.STAR, radius=1), "stencil_generic_kernel", 1),
+        (B.make_desc(3, (256,) * 3, shape=B.STAR, radius=4, temporal_depth=2),
+         "stencil_star_tb2_kernel", 2),
+    ]
+    for d, kernel, depth in cases:
+        h = B.stencil_plan(d)
+        info = B.stencil_plan_query(h)
+        assert info.kernel.decode() == kernel and info.temporal_depth == depth
+        B.stencil_destroy(h)
+
+
 def test_plan_and_query_without_gpu():
-    h = B.stencil_plan(B.make_desc(2, (16, 16), shape=B.BOX, radius=3, dtype=B.F64))
+    h = B.stencil_plan(B.make_desc(2, (16, 18), shape=B.BOX, radius=3, dtype=B.F64))
     info = B.stencil_plan_query(h)
     assert info.variant == B.VARIANT_GENERIC and info.temporal_depth == 1
-    assert info.scratch_bytes == 16 * 16 * 8
+    assert info.scratch_bytes == 16 * 18 * 8
     assert info.kernel.decode() == "stencil_generic_kernel"
     B.stencil_destroy(h)
     B.stencil_destroy(None)

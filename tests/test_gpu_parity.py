@@ -216,3 +216,44 @@ def test_fused_steps_match_single_steps():
     report("fused", fused, ref, tolerance(wl, x))
     report("single", single, ref, tolerance(wl, x))
     assert np.abs(fused - single).max() <= 2 * tolerance(wl, x)
+
+
+BOX2_CASES = [(R, dt, bnd) for R in (1, 2, 3, 4) for dt in ("f32", "f64")
+              for bnd in (B.ZERO, B.PERIODIC)]
+
+
+@pytest.mark.parametrize("R,dt,bnd", BOX2_CASES,
+                         ids=["R%d-%s-%s" % (c[0], c[1], "zero" if c[2] == 0 else "per")
+                              for c in BOX2_CASES])
+@pytest.mark.parametrize("nx", [512, 32], ids=["wide", "narrow"])
+def test_box2d_radius_dtype_boundary(R, dt, bnd, nx):
+    """2D boxes (the paper's operator family): every radius up to 4, fp32 and fp64, both
+    boundaries, rows that span several 64-lane segments or several rows per wavefront,
+    a ragged row count and 3 steps, batch 3 with 2 weight sets."""
+    from dataclasses import replace
+    g = np.random.default_rng(200 + R)
+    wl = replace(WORKLOADS["paper"].resized((131, nx), steps=3), radius=R, boundary=bnd,
+                 dtype=dt, batch=3, channels=2)
+    npdt = np.float32 if dt == "f32" else np.float64
+    x = g.uniform(-1, 1, (3, 131, nx)).astype(npdt)
+    w = g.uniform(-1, 1, (2, wl.npoints))
+    w = (w / np.abs(w).sum(axis=1, keepdims=True)).astype(npdt)
+    got, info = run_library(wl, x, w)
+    assert info["kernel"] == "stencil_box2_stream_kernel", info
+    ref = oracle_full(wl, x, w)
+    report("box2d R=%d %s bnd=%d nx=%d" % (R, dt, bnd, nx), got, ref, tolerance(wl, x))
+
+
+def test_paper_workload_full_size_sampled():
+    """The paper's own case: 2D 49-point box, radius 3, 10240 x 10240 fp64, zero padding,
+    a few steps of the iteration, sampled against the oracle."""
+    wl = WORKLOADS["paper"].resized((10240, 10240), steps=3)
+    x, w, _ = inputs.make(wl)
+    got, info = run_library(wl, x, w)
+    print("[info] %s" % info, flush=True)
+    assert info["kernel"] == "stencil_box2_stream_kernel"
+    pts = sample_points(wl, x, 300, seed=2)
+    ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                              steps=wl.steps, ndim=2)
+    report("paper full (%d samples)" % len(pts), gather(got, pts, wl), ref, tolerance(wl, x))
+    assert np.isfinite(got).all()
