@@ -194,6 +194,42 @@ def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
     return {"bytes": nbytes, "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}
 
 
+def miopen_context(torch, wl, x_host, w, reps=5):
+    """Time torch's convolution (MIOpen on ROCm) on the same workload, one stencil step per
+    call: the MI355X counterpart of the paper's cuDNN dense reference.  Context only; its
+    result is never a parity reference.  Returns None if MIOpen cannot run the case."""
+    try:
+        F = torch.nn.functional
+        dev = torch.device("cuda:0")
+        x = torch.from_numpy(x_host).to(dev)
+        k = 2 * wl.radius + 1
+        if wl.ndim == 2:
+            inp = x.reshape(1, 1, *wl.dims)
+            wt = torch.from_numpy(w.reshape(1, 1, k, k)).to(dev)
+            run = lambda: F.conv2d(inp, wt, padding=wl.radius)
+        else:
+            inp = x.reshape(wl.n, wl.channels, *wl.dims)
+            wt = torch.from_numpy(w.reshape(wl.channels, 1, k, k, k)).to(dev)
+            run = lambda: F.conv3d(inp, wt, padding=wl.radius, groups=wl.channels)
+        for _ in range(2):
+            run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        e1.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        del inp, wt, x
+        torch.cuda.empty_cache()
+        return {"ms_per_step": round(ms, 4),
+                "gpoints_per_s": round(wl.points_per_step / (ms * 1e-3) / 1e9, 2),
+                "what": "torch.nn.functional.conv%dd (MIOpen), one step, same input" % wl.ndim}
+    except Exception as e:  # MIOpen may not support every dtype/shape
+        return {"error": str(e)[:200]}
+
+
 def cpu_baseline(wl, x_host, w, planes: int):
     """The fp64 oracle, single-threaded, on a z-slab of the headline input."""
     import oracle
@@ -298,6 +334,8 @@ def main() -> int:
             if name == "paper":
                 rec["ms_per_stencil_step"] = round(t / w2.steps, 5)
                 rec["context_a100_ms_per_step"] = PAPER_A100_MS_PER_STEP
+            if name in ("paper", "c5"):
+                rec["context_miopen"] = miopen_context(torch, w2, r.x_host, r.w)
             others[name] = rec
             log("[bench] %s: %s" % (name, rec))
             r.close()

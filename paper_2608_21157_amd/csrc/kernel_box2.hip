@@ -106,17 +106,20 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
             ho[k] = (ok && hok[k]) ? (y * p.nx + hx[k]) * E : kOutOfRange;
     };
 
-    // rolling queue of PF input rows (row k of the chunk's input is slot k mod PF)
-    Vec16<T> qv[PF], qh[PF][HXV];
+    // rolling queue of PF input rows (row k of the chunk's input is slot k mod PF); the
+    // halo vectors (used by two lanes of the segment) are read one row ahead
+    Vec16<T> qv[PF], hcur[HXV], hnxt[HXV];
     const int nin = p.yc + 2 * R;  // input rows y0 - R .. y0 + yc - 1 + R
 #pragma unroll
     for (int s = 0; s < PF; ++s) {
         int own, ho[HXV];
         row_off(y0 - R + s, own, ho);
         qv[s] = bload16<T>(rin, s < nin ? own : kOutOfRange);
+        if (s == 0) {
 #pragma unroll
-        for (int k = 0; k < HXV; ++k)
-            qh[s][k] = bload16<T>(rin, s < nin ? ho[k] : kOutOfRange);
+            for (int k = 0; k < HXV; ++k)
+                hnxt[k] = bload16<T>(rin, ho[k]);
+        }
     }
 
     T acc[NS][VEC];
@@ -131,6 +134,16 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
     // q mod NS.  Rows q outside [0, yc) are skipped (uniform across the wavefront).
     auto fold = [&](int k, int pslot, auto slot_of_q) {
         const Vec16<T> own = qv[pslot];
+#pragma unroll
+        for (int j = 0; j < HXV; ++j)
+            hcur[j] = hnxt[j];
+        if (k + 1 < nin) {
+            int o1, h1[HXV];
+            row_off(y0 - R + k + 1, o1, h1);
+#pragma unroll
+            for (int j = 0; j < HXV; ++j)
+                hnxt[j] = bload16<T>(rin, h1[j]);
+        }
         // extended row: vectors of lanes -HXV .. +HXV (halo at the segment's ends)
         Vec16<T> lft[HXV], rgt[HXV];
 #pragma unroll
@@ -139,10 +152,10 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
             const Vec16<T> &sr = j == 0 ? own : rgt[j - 1];
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
-                const T l = from_left_lane(sl.e[e], qh[pslot][j].e[e]);
-                const T r = from_right_lane(sr.e[e], qh[pslot][j].e[e]);
-                lft[j].e[e] = first ? qh[pslot][j].e[e] : l;
-                rgt[j].e[e] = last ? qh[pslot][j].e[e] : r;
+                const T l = from_left_lane(sl.e[e], hcur[j].e[e]);
+                const T r = from_right_lane(sr.e[e], hcur[j].e[e]);
+                lft[j].e[e] = first ? hcur[j].e[e] : l;
+                rgt[j].e[e] = last ? hcur[j].e[e] : r;
             }
         }
         T ext[NX];
@@ -161,9 +174,6 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
             int o2, h2[HXV];
             row_off(y0 - R + k + PF, o2, h2);
             qv[pslot] = bload16<T>(rin, o2);
-#pragma unroll
-            for (int j = 0; j < HXV; ++j)
-                qh[pslot][j] = bload16<T>(rin, h2[j]);
         }
 #pragma unroll
         for (int a = 0; a < NW; ++a) {
@@ -201,6 +211,227 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
             if (k >= nin)
                 break;
             fold(k, j, [j](int a) { return ((j - a) % NS + NS) % NS; });
+        }
+    }
+}
+
+// Two steps of the 2D box in one pass.  A wavefront's 64 lanes cover a virtual x range
+// that starts HXV vectors left of its output columns and ends HXV vectors right of them:
+// stage 1 computes u1 on all 64 lanes (the first and last lanes read the u0 halo beyond the
+// range), stage 2 folds each completed u1 row into its own accumulators with the lane
+// shifts, and only the inner 64 - 2 HXV lanes, whose u1 neighbours are all inside the
+// wavefront, are written.  Consecutive wavefronts overlap by 2 HXV lanes.  Under the zero
+// boundary u1 is zero outside the grid, exactly as if it had been written and re-read.
+// Input row k feeds u1 row k - a (both relative to the chunk), which feeds u2 row
+// (k - 2R) - a; with the input queue, both accumulator sets rotate with period 2R + 1.
+template <typename T, int R, bool PERIODIC, int STORE_CP>
+__global__ __launch_bounds__(256) void stencil_box2_tb2_kernel(
+    const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, Box2Params p)
+{
+    constexpr int VEC = Vec16<T>::N;
+    constexpr int E = sizeof(T);
+    constexpr int HXV = (R + VEC - 1) / VEC;
+    constexpr int NS = 2 * R + 1;
+    constexpr int NW = 2 * R + 1;
+    constexpr int NX = (2 * HXV + 1) * VEC;
+    constexpr int PF = NS;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    const long long tw = (long long)xcd_logical_block(blockIdx.x, p.nblocks) * 4 + wave;
+    const int units = p.segs * p.nyc;
+    const long long b = tw / units;
+    if (b >= p.batch)
+        return;  // whole wavefront leaves; the kernel has no barriers
+    const int t = int(tw - b * units);
+    const int seg = t % p.segs;
+    const int ch = t / p.segs;
+    const int xs = seg * p.segw - HXV * VEC;  // virtual x of lane 0 (p.segw: output width)
+    const int x = xs + lane * VEC;
+    const bool xin = x >= 0 && x < p.nx;
+    const bool out_lane = xin && lane >= HXV && lane < 64 - HXV;
+    const int y0 = ch * p.yc;
+    const int n = max(0, min(p.yc, p.ny - y0));
+    const T *src = in + b * p.vol;
+    T *dst = out + b * p.vol;
+    const unsigned img_bytes = unsigned(p.vol * E);
+    const auto rin = make_rsrc(src, img_bytes);
+    const auto rout = make_rsrc(dst, img_bytes);
+    const T *wb = w + (b % p.channels) * (NW * NW);
+
+    const bool first = lane == 0, last = lane == 63;
+    auto wrap_x = [&](int xx, bool &ok) {
+        ok = xx >= 0 && xx < p.nx;
+        if (PERIODIC) {
+            xx = wrap_index(xx, p.nx);
+            ok = true;
+        }
+        return xx;
+    };
+    bool own_ok;
+    const int xo = wrap_x(x, own_ok);
+    int hx[HXV];
+    bool hok[HXV];
+#pragma unroll
+    for (int k = 0; k < HXV; ++k) {
+        hx[k] = wrap_x(first ? xs - (k + 1) * VEC : xs + 64 * VEC + k * VEC, hok[k]);
+        hok[k] = hok[k] && (first || last);
+    }
+    auto row_off = [&](int y, int &own, int (&ho)[HXV]) {
+        bool ok = y >= 0 && y < p.ny;
+        if (PERIODIC) {
+            y = wrap_index(y, p.ny);
+            ok = true;
+        }
+        own = (ok && own_ok) ? (y * p.nx + xo) * E : kOutOfRange;
+#pragma unroll
+        for (int k = 0; k < HXV; ++k)
+            ho[k] = (ok && hok[k]) ? (y * p.nx + hx[k]) * E : kOutOfRange;
+    };
+
+    // input rows y0 - 2R .. y0 + yc - 1 + 2R; u1 rows y0 - R .. y0 + yc - 1 + R
+    const int nin = p.yc + 4 * R;
+    const int n1 = p.yc + 2 * R;
+    Vec16<T> qv[PF], hcur[HXV], hnxt[HXV];
+#pragma unroll
+    for (int s = 0; s < PF; ++s) {
+        int own, ho[HXV];
+        row_off(y0 - 2 * R + s, own, ho);
+        qv[s] = bload16<T>(rin, own);
+        if (s == 0) {
+#pragma unroll
+            for (int k = 0; k < HXV; ++k)
+                hnxt[k] = bload16<T>(rin, ho[k]);
+        }
+    }
+    T acc1[NS][VEC], acc2[NS][VEC];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            acc1[s][e] = T(0);
+            acc2[s][e] = T(0);
+        }
+
+    // the 2 HXV + 1 vectors around this lane: DPP shifts, `fix` supplies lane 0's left and
+    // lane 63's right neighbours (the u0 halo; unused for u1)
+    auto extend = [&](const Vec16<T> &own, const Vec16<T>(&fix)[HXV], bool use_fix,
+                      T(&ext)[NX]) {
+        Vec16<T> lft[HXV], rgt[HXV];
+#pragma unroll
+        for (int j = 0; j < HXV; ++j) {
+            const Vec16<T> &sl = j == 0 ? own : lft[j - 1];
+            const Vec16<T> &sr = j == 0 ? own : rgt[j - 1];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const T l = from_left_lane(sl.e[e], fix[j].e[e]);
+                const T r = from_right_lane(sr.e[e], fix[j].e[e]);
+                lft[j].e[e] = (use_fix && first) ? fix[j].e[e] : l;
+                rgt[j].e[e] = (use_fix && last) ? fix[j].e[e] : r;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < HXV; ++j)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                ext[(HXV - 1 - j) * VEC + e] = lft[j].e[e];
+                ext[(HXV + 1 + j) * VEC + e] = rgt[j].e[e];
+            }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            ext[HXV * VEC + e] = own.e[e];
+    };
+
+    auto step = [&](int k, int j) {
+        // ---- stage 1: input row k -------------------------------------------------
+        const Vec16<T> own = qv[j];
+#pragma unroll
+        for (int i = 0; i < HXV; ++i)
+            hcur[i] = hnxt[i];
+        if (k + 1 < nin) {
+            int o1, h1[HXV];
+            row_off(y0 - 2 * R + k + 1, o1, h1);
+#pragma unroll
+            for (int i = 0; i < HXV; ++i)
+                hnxt[i] = bload16<T>(rin, h1[i]);
+        }
+        T ext[NX];
+        extend(own, hcur, true, ext);
+        if (k + PF < nin) {
+            int o2, h2[HXV];
+            row_off(y0 - 2 * R + k + PF, o2, h2);
+            qv[j] = bload16<T>(rin, o2);
+        }
+#pragma unroll
+        for (int a = 0; a < NW; ++a) {
+            const int r1 = k - a;
+            if (r1 < 0 || r1 >= n1)
+                continue;
+            const int s = ((j - a) % NS + NS) % NS;
+#pragma unroll
+            for (int c = 0; c < NW; ++c) {
+                const T wv = wb[a * NW + c];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc1[s][e] = fma(wv, ext[HXV * VEC + e + c - R], acc1[s][e]);
+            }
+        }
+        // ---- u1 row k - 2R is complete: fold it into stage 2 ---------------------------
+        const int r1 = k - 2 * R;
+        if (r1 < 0 || r1 >= n1)
+            return;
+        const int s1 = (j + 1) % NS;
+        Vec16<T> u1;
+        const int y1 = y0 - R + r1;
+        const bool keep = PERIODIC || (xin && y1 >= 0 && y1 < p.ny);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            u1.e[e] = keep ? acc1[s1][e] : T(0);
+            acc1[s1][e] = T(0);
+        }
+        T ext2[NX];
+        Vec16<T> nofix[HXV];
+#pragma unroll
+        for (int i = 0; i < HXV; ++i)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                nofix[i].e[e] = T(0);
+        extend(u1, nofix, false, ext2);
+#pragma unroll
+        for (int a = 0; a < NW; ++a) {
+            const int r2 = r1 - a;
+            if (r2 < 0 || r2 >= p.yc)
+                continue;
+            const int s = ((j + 1 - a) % NS + NS) % NS;
+#pragma unroll
+            for (int c = 0; c < NW; ++c) {
+                const T wv = wb[a * NW + c];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc2[s][e] = fma(wv, ext2[HXV * VEC + e + c - R], acc2[s][e]);
+            }
+        }
+        // ---- u2 row k - 4R is complete ------------------------------------------
+        const int r2 = k - 4 * R;
+        if (r2 >= 0 && r2 < p.yc) {
+            const int s2 = (j + 2) % NS;
+            Vec16<T> v;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                v.e[e] = acc2[s2][e];
+                acc2[s2][e] = T(0);
+            }
+            bstore16<T, STORE_CP>(rout, (out_lane && r2 < n) ? ((y0 + r2) * p.nx + x) * E
+                                                              : kOutOfRange, v);
+        }
+    };
+
+    for (int k0 = 0; k0 < nin; k0 += NS) {
+#pragma unroll
+        for (int j = 0; j < NS; ++j) {
+            if (k0 + j >= nin)
+                break;
+            step(k0 + j, j);
         }
     }
 }
@@ -256,6 +487,53 @@ Box2Params make_params(const Geometry &g)
     return p;
 }
 
+template <typename T, int R>
+Box2Params make_tb2_params(const Geometry &g)
+{
+    constexpr int VEC = Vec16<T>::N;
+    constexpr int HXV = (R + VEC - 1) / VEC;
+    Box2Params p{};
+    p.ny = int(g.ny);
+    p.nx = int(g.nx);
+    p.vol = g.vol;
+    p.lpr = 64;
+    p.segw = (64 - 2 * HXV) * VEC;  // output columns per wavefront
+    p.segs = int((g.nx + p.segw - 1) / p.segw);
+    p.rg = 1;
+    p.batch = g.batch;
+    p.channels = g.channels;
+    const long long target = env_int("STENCIL_BOX2_TARGET_WAVES", 4096);
+    const long long per_image = g.batch * p.segs;
+    long long nchunks = (target + per_image - 1) / per_image;
+    const long long max_chunks = (p.ny + 32 * R - 1) / (32 * R);  // >= 32R rows per chunk
+    if (nchunks > max_chunks)
+        nchunks = max_chunks;
+    if (nchunks < 1)
+        nchunks = 1;
+    p.yc = int((p.ny + nchunks - 1) / nchunks);
+    p.nyc = (p.ny + p.yc - 1) / p.yc;
+    const long long waves = g.batch * p.segs * p.nyc;
+    p.nblocks = int((waves + 3) / 4);
+    return p;
+}
+
+template <typename T, int R, int CP>
+hipError_t launch_tb2_cp(const Geometry &g, const void *src, void *dst, const void *w,
+                         hipStream_t stream)
+{
+    const Box2Params p = make_tb2_params<T, R>(g);
+    const T *s = static_cast<const T *>(src);
+    T *d = static_cast<T *>(dst);
+    const T *wt = static_cast<const T *>(w);
+    if (g.boundary == STENCIL_PERIODIC)
+        stencil_box2_tb2_kernel<T, R, true, CP>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    else
+        stencil_box2_tb2_kernel<T, R, false, CP>
+            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    return hipGetLastError();
+}
+
 template <typename T, int R, int CP>
 hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)
@@ -274,23 +552,26 @@ hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *
 }
 
 template <typename T, int R>
-hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w,
+hipError_t launch_r(const Geometry &g, const void *src, void *dst, const void *w, int depth,
                     hipStream_t stream)
 {
-    if (streaming_stores(g))
-        return launch_cp<T, R, kNonTemporal>(g, src, dst, w, stream);
-    return launch_cp<T, R, 0>(g, src, dst, w, stream);
+    const bool nt = streaming_stores(g);
+    if (depth == 2)
+        return nt ? launch_tb2_cp<T, R, kNonTemporal>(g, src, dst, w, stream)
+                  : launch_tb2_cp<T, R, 0>(g, src, dst, w, stream);
+    return nt ? launch_cp<T, R, kNonTemporal>(g, src, dst, w, stream)
+              : launch_cp<T, R, 0>(g, src, dst, w, stream);
 }
 
 template <typename T>
-hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *w,
+hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *w, int depth,
                     hipStream_t stream)
 {
     switch (g.radius) {
-    case 1: return launch_r<T, 1>(g, src, dst, w, stream);
-    case 2: return launch_r<T, 2>(g, src, dst, w, stream);
-    case 3: return launch_r<T, 3>(g, src, dst, w, stream);
-    case 4: return launch_r<T, 4>(g, src, dst, w, stream);
+    case 1: return launch_r<T, 1>(g, src, dst, w, depth, stream);
+    case 2: return launch_r<T, 2>(g, src, dst, w, depth, stream);
+    case 3: return launch_r<T, 3>(g, src, dst, w, depth, stream);
+    case 4: return launch_r<T, 4>(g, src, dst, w, depth, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -309,12 +590,18 @@ bool box2_stream_supported(const Geometry &g)
            g.batch * (g.nx / vec) < (int64_t(1) << 30);
 }
 
+bool box2_tb2_supported(const Geometry &g)
+{
+    // the one-step kernel must also run the shape: odd step counts end with a single step
+    return box2_stream_supported(g);
+}
+
 hipError_t launch_box2_stream(const Geometry &g, const void *src, void *dst, const void *w,
-                              hipStream_t stream)
+                              int depth, hipStream_t stream)
 {
     if (g.dtype == STENCIL_F32)
-        return launch_t<float>(g, src, dst, w, stream);
-    return launch_t<double>(g, src, dst, w, stream);
+        return launch_t<float>(g, src, dst, w, depth, stream);
+    return launch_t<double>(g, src, dst, w, depth, stream);
 }
 
 }  // namespace stencil

@@ -5,12 +5,13 @@ namespace stencil {
 
 bool stream_supported(const Geometry &g)
 {
-    return box_stream_supported(g) || box2_stream_supported(g) || star_stream_supported(g);
+    return box_stream_supported(g) || box2_stream_supported(g) || box2_tb2_supported(g) ||
+           star_stream_supported(g);
 }
 
 int stream_max_depth(const Geometry &g)
 {
-    return star_tb2_supported(g) ? 2 : 1;
+    return (star_tb2_supported(g) || box2_tb2_supported(g)) ? 2 : 1;
 }
 
 int stream_default_depth(const Geometry &g)
@@ -19,6 +20,9 @@ int stream_default_depth(const Geometry &g)
     // bands and LDS traffic that grow with the radius.  Measured on MI355X (512^3 and 256^3
     // fp32): a clear win at radius 1, no gain at radius 4, where one step per launch is
     // already close to the streaming-copy ceiling.
+    // 2D boxes: two steps per pass measured 1.26x faster per step (10240^2 fp64, radius 3)
+    if (box2_tb2_supported(g))
+        return 2;
     return (star_tb2_supported(g) && g.radius <= 2) ? 2 : 1;
 }
 
@@ -26,6 +30,8 @@ const char *stream_kernel_name(const Geometry &g, int depth)
 {
     if (box_stream_supported(g))
         return "stencil_box3_stream_kernel";
+    if (box2_tb2_supported(g) && depth == 2)
+        return "stencil_box2_tb2_kernel";
     if (box2_stream_supported(g))
         return "stencil_box2_stream_kernel";
     if (star_tb2_supported(g) && depth == 2)
@@ -40,12 +46,14 @@ hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const vo
 {
     if (depth == 2 && star_tb2_supported(g))
         return launch_star_tb2(g, src, dst, w, stream);
+    if (depth == 2 && box2_tb2_supported(g))
+        return launch_box2_stream(g, src, dst, w, 2, stream);
     if (depth != 1)
         return hipErrorInvalidValue;
     if (box_stream_supported(g))
         return launch_box_stream(g, src, dst, field, w, stream);
     if (box2_stream_supported(g))
-        return launch_box2_stream(g, src, dst, w, stream);
+        return launch_box2_stream(g, src, dst, w, 1, stream);
     if (star_stream_supported(g))
         return launch_star_stream(g, src, dst, w, stream);
     return hipErrorInvalidValue;

@@ -69,8 +69,9 @@ hipError_t launch_star_stream(const Geometry &g, const void *src, void *dst, con
                               hipStream_t stream);
 
 bool box2_stream_supported(const Geometry &g);
+bool box2_tb2_supported(const Geometry &g);
 hipError_t launch_box2_stream(const Geometry &g, const void *src, void *dst, const void *w,
-                              hipStream_t stream);
+                              int depth, hipStream_t stream);
 
 // Two star steps fused in one pass (3D).
 bool star_tb2_supported(const Geometry &g);

@@ -109,6 +109,8 @@ def test_planner_choices():
         (B.make_desc(3, (128,) * 3, batch=256, channels=32, shape=B.BOX, radius=1),
          "stencil_box3_stream_kernel", 1),
         (B.make_desc(2, (10240, 10240), shape=B.BOX, radius=3, dtype=B.F64),
+         "stencil_box2_tb2_kernel", 2),
+        (B.make_desc(2, (10240, 10240), shape=B.BOX, radius=3, dtype=B.F64, temporal_depth=1),
          "stencil_box2_stream_kernel", 1),
         (B.make_desc(2, (256, 256), shape=B.STAR, radius=1), "stencil_star_stream_kernel", 1),
         (B.make_desc(3, (8, 8, 10), shape=B.STAR, radius=1), "stencil_generic_kernel", 1),

@@ -226,7 +226,8 @@ BOX2_CASES = [(R, dt, bnd) for R in (1, 2, 3, 4) for dt in ("f32", "f64")
                          ids=["R%d-%s-%s" % (c[0], c[1], "zero" if c[2] == 0 else "per")
                               for c in BOX2_CASES])
 @pytest.mark.parametrize("nx", [512, 32], ids=["wide", "narrow"])
-def test_box2d_radius_dtype_boundary(R, dt, bnd, nx):
+@pytest.mark.parametrize("depth", [1, 0], ids=["depth1", "auto"])
+def test_box2d_radius_dtype_boundary(R, dt, bnd, nx, depth):
     """2D boxes (the paper's operator family): every radius up to 4, fp32 and fp64, both
     boundaries, rows that span several 64-lane segments or several rows per wavefront,
     a ragged row count and 3 steps, batch 3 with 2 weight sets."""
@@ -238,10 +239,11 @@ def test_box2d_radius_dtype_boundary(R, dt, bnd, nx):
     x = g.uniform(-1, 1, (3, 131, nx)).astype(npdt)
     w = g.uniform(-1, 1, (2, wl.npoints))
     w = (w / np.abs(w).sum(axis=1, keepdims=True)).astype(npdt)
-    got, info = run_library(wl, x, w)
-    assert info["kernel"] == "stencil_box2_stream_kernel", info
+    got, info = run_library(wl, x, w, depth=depth)
+    assert info["kernel"] in ("stencil_box2_stream_kernel", "stencil_box2_tb2_kernel"), info
     ref = oracle_full(wl, x, w)
-    report("box2d R=%d %s bnd=%d nx=%d" % (R, dt, bnd, nx), got, ref, tolerance(wl, x))
+    report("box2d R=%d %s bnd=%d nx=%d %s" % (R, dt, bnd, nx, info), got, ref,
+           tolerance(wl, x))
 
 
 def test_paper_workload_full_size_sampled():
@@ -251,7 +253,7 @@ def test_paper_workload_full_size_sampled():
     x, w, _ = inputs.make(wl)
     got, info = run_library(wl, x, w)
     print("[info] %s" % info, flush=True)
-    assert info["kernel"] == "stencil_box2_stream_kernel"
+    assert info["kernel"] in ("stencil_box2_stream_kernel", "stencil_box2_tb2_kernel")
     pts = sample_points(wl, x, 300, seed=2)
     ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
                               steps=wl.steps, ndim=2)
