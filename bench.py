@@ -39,6 +39,8 @@ KERNEL_SOURCES = {
     "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp"],
     "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp"],
     "stencil_star_tb2_kernel": ["kernel_star_tb.hip", "common.hpp"],
+    "stencil_box2_stream_kernel": ["kernel_box2.hip", "common.hpp"],
+    "stencil_box2_tb2_kernel": ["kernel_box2.hip", "common.hpp"],
     "stencil_generic_kernel": ["kernel_generic.hip"],
 }
 
@@ -256,6 +258,8 @@ def main() -> int:
     ap.add_argument("--no-others", action="store_true", help="headline workload only")
     ap.add_argument("--cpu-planes", type=int, default=320,
                     help="z planes of the headline input the CPU oracle runs on (~10-20 s)")
+    ap.add_argument("--stencil-steps", type=int, default=0,
+                    help="override the workload's stencil steps per call (profiling runs)")
     ap.add_argument("--depth", type=int, default=0,
                     help="stencil steps fused per launch (0: the planner's choice)")
     ap.add_argument("--copy-only", action="store_true",
@@ -282,6 +286,8 @@ def main() -> int:
         print(json.dumps({"copy_probe": probe}), flush=True)
         return 0
     wl = inputs.WORKLOADS[args.workload]
+    if args.stencil_steps > 0:
+        wl = wl.resized(wl.dims, steps=args.stencil_steps)
 
     head = Runner(torch, B, inputs, wl, stream, depth=args.depth)
     ms_total = head.timed(args.steps, args.warmup)
