@@ -170,10 +170,10 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
                 r[e + 1] = rows[i].e[e];
-            if (more) {
-                rows[i] = bload16<T>(rn, ro[i]);
-                halo[i] = bload1(rn, ho[i], T(0));
-            }
+            // unconditional (an offset past the resource after the last plane): a load
+            // under a branch would make the compiler's wait counts conservative
+            rows[i] = bload16<T>(rn, more ? ro[i] : kOutOfRange);
+            halo[i] = bload1(rn, more ? ho[i] : kOutOfRange, T(0));
 #pragma unroll
             for (int a = 0; a < 3; ++a) {
                 if (k - a < 0 || k - a >= n)

@@ -137,12 +137,12 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
 #pragma unroll
         for (int j = 0; j < HXV; ++j)
             hcur[j] = hnxt[j];
-        if (k + 1 < nin) {
+        {
             int o1, h1[HXV];
             row_off(y0 - R + k + 1, o1, h1);
 #pragma unroll
             for (int j = 0; j < HXV; ++j)
-                hnxt[j] = bload16<T>(rin, h1[j]);
+                hnxt[j] = bload16<T>(rin, k + 1 < nin ? h1[j] : kOutOfRange);
         }
         // extended row: vectors of lanes -HXV .. +HXV (halo at the segment's ends)
         Vec16<T> lft[HXV], rgt[HXV];
@@ -170,10 +170,10 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
         for (int e = 0; e < VEC; ++e)
             ext[HXV * VEC + e] = own.e[e];
         // refill the slot with input row k + PF
-        if (k + PF < nin) {
+        {
             int o2, h2[HXV];
             row_off(y0 - R + k + PF, o2, h2);
-            qv[pslot] = bload16<T>(rin, o2);
+            qv[pslot] = bload16<T>(rin, k + PF < nin ? o2 : kOutOfRange);
         }
 #pragma unroll
         for (int a = 0; a < NW; ++a) {
@@ -189,9 +189,10 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
                     acc[s][e] = fma(wv, ext[HXV * VEC + e + c - R], acc[s][e]);
             }
         }
-        // output row k - 2R is complete
+        // output row k - 2R is complete (rows before the chunk never received a
+        // contribution, so the slot is cleared whatever the row)
         const int qd = k - 2 * R;
-        if (qd >= 0 && qd < p.yc) {
+        {
             const int sd = slot_of_q(2 * R);
             Vec16<T> v;
 #pragma unroll
@@ -199,20 +200,24 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
                 v.e[e] = acc[sd][e];
                 acc[sd][e] = T(0);
             }
-            bstore16<T, STORE_CP>(rout, qd < n ? ((y0 + qd) * p.nx + x) * E : kOutOfRange, v);
+            bstore16<T, STORE_CP>(
+                rout, (qd >= 0 && qd < n) ? ((y0 + qd) * p.nx + x) * E : kOutOfRange, v);
         }
     };
 
-    // unrolled NS times (PF = NS) so that queue and accumulator slots are static
-    for (int k0 = 0; k0 < nin; k0 += NS) {
+    // unrolled NS times (PF = NS) so that queue and accumulator slots are static; whole
+    // groups in the loop, the remainder after it (an early exit inside the loop body would
+    // merge into the loop head and make its waits conservative)
+    int k0 = 0;
+    for (; k0 + NS <= nin; k0 += NS) {
 #pragma unroll
-        for (int j = 0; j < NS; ++j) {
-            const int k = k0 + j;
-            if (k >= nin)
-                break;
-            fold(k, j, [j](int a) { return ((j - a) % NS + NS) % NS; });
-        }
+        for (int j = 0; j < NS; ++j)
+            fold(k0 + j, j, [j](int a) { return ((j - a) % NS + NS) % NS; });
     }
+#pragma unroll
+    for (int j = 0; j < NS - 1; ++j)
+        if (k0 + j < nin)
+            fold(k0 + j, j, [j](int a) { return ((j - a) % NS + NS) % NS; });
 }
 
 // Two steps of the 2D box in one pass.  A wavefront's 64 lanes cover a virtual x range
@@ -342,44 +347,9 @@ __global__ __launch_bounds__(256) void stencil_box2_tb2_kernel(
             ext[HXV * VEC + e] = own.e[e];
     };
 
-    auto step = [&](int k, int j) {
-        // ---- stage 1: input row k -------------------------------------------------
-        const Vec16<T> own = qv[j];
-#pragma unroll
-        for (int i = 0; i < HXV; ++i)
-            hcur[i] = hnxt[i];
-        if (k + 1 < nin) {
-            int o1, h1[HXV];
-            row_off(y0 - 2 * R + k + 1, o1, h1);
-#pragma unroll
-            for (int i = 0; i < HXV; ++i)
-                hnxt[i] = bload16<T>(rin, h1[i]);
-        }
-        T ext[NX];
-        extend(own, hcur, true, ext);
-        if (k + PF < nin) {
-            int o2, h2[HXV];
-            row_off(y0 - 2 * R + k + PF, o2, h2);
-            qv[j] = bload16<T>(rin, o2);
-        }
-#pragma unroll
-        for (int a = 0; a < NW; ++a) {
-            const int r1 = k - a;
-            if (r1 < 0 || r1 >= n1)
-                continue;
-            const int s = ((j - a) % NS + NS) % NS;
-#pragma unroll
-            for (int c = 0; c < NW; ++c) {
-                const T wv = wb[a * NW + c];
-#pragma unroll
-                for (int e = 0; e < VEC; ++e)
-                    acc1[s][e] = fma(wv, ext[HXV * VEC + e + c - R], acc1[s][e]);
-            }
-        }
-        // ---- u1 row k - 2R is complete: fold it into stage 2 ---------------------------
-        const int r1 = k - 2 * R;
-        if (r1 < 0 || r1 >= n1)
-            return;
+    // stage 2: fold completed u1 row r1 (in accumulator slot (j + 1) mod NS) into the u2
+    // accumulators; arithmetic only, so the caller's branch around it holds no memory access
+    auto fold2 = [&](int j, int r1) {
         const int s1 = (j + 1) % NS;
         Vec16<T> u1;
         const int y1 = y0 - R + r1;
@@ -411,9 +381,50 @@ __global__ __launch_bounds__(256) void stencil_box2_tb2_kernel(
                     acc2[s][e] = fma(wv, ext2[HXV * VEC + e + c - R], acc2[s][e]);
             }
         }
-        // ---- u2 row k - 4R is complete ------------------------------------------
+    };
+
+    auto step = [&](int k, int j) {
+        // ---- stage 1: input row k -------------------------------------------------
+        const Vec16<T> own = qv[j];
+#pragma unroll
+        for (int i = 0; i < HXV; ++i)
+            hcur[i] = hnxt[i];
+        {
+            int o1, h1[HXV];
+            row_off(y0 - 2 * R + k + 1, o1, h1);
+#pragma unroll
+            for (int i = 0; i < HXV; ++i)
+                hnxt[i] = bload16<T>(rin, k + 1 < nin ? h1[i] : kOutOfRange);
+        }
+        T ext[NX];
+        extend(own, hcur, true, ext);
+        {
+            int o2, h2[HXV];
+            row_off(y0 - 2 * R + k + PF, o2, h2);
+            qv[j] = bload16<T>(rin, k + PF < nin ? o2 : kOutOfRange);
+        }
+#pragma unroll
+        for (int a = 0; a < NW; ++a) {
+            const int r1 = k - a;
+            if (r1 < 0 || r1 >= n1)
+                continue;
+            const int s = ((j - a) % NS + NS) % NS;
+#pragma unroll
+            for (int c = 0; c < NW; ++c) {
+                const T wv = wb[a * NW + c];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc1[s][e] = fma(wv, ext[HXV * VEC + e + c - R], acc1[s][e]);
+            }
+        }
+        // ---- u1 row k - 2R is complete: fold it into stage 2 ---------------------------
+        const int r1 = k - 2 * R;
+        if (r1 >= 0 && r1 < n1)
+            fold2(j, r1);
+        // ---- u2 row k - 4R is complete (rows before the chunk never received a
+        // contribution, so the slot is cleared whatever the row) --------------------------
         const int r2 = k - 4 * R;
-        if (r2 >= 0 && r2 < p.yc) {
+        {
             const int s2 = (j + 2) % NS;
             Vec16<T> v;
 #pragma unroll
@@ -421,19 +432,22 @@ __global__ __launch_bounds__(256) void stencil_box2_tb2_kernel(
                 v.e[e] = acc2[s2][e];
                 acc2[s2][e] = T(0);
             }
-            bstore16<T, STORE_CP>(rout, (out_lane && r2 < n) ? ((y0 + r2) * p.nx + x) * E
-                                                              : kOutOfRange, v);
+            bstore16<T, STORE_CP>(rout, (out_lane && r2 >= 0 && r2 < n)
+                                            ? ((y0 + r2) * p.nx + x) * E : kOutOfRange, v);
         }
     };
 
-    for (int k0 = 0; k0 < nin; k0 += NS) {
+    // whole groups in the loop, the remainder after it (as in the one-step kernel)
+    int k0 = 0;
+    for (; k0 + NS <= nin; k0 += NS) {
 #pragma unroll
-        for (int j = 0; j < NS; ++j) {
-            if (k0 + j >= nin)
-                break;
+        for (int j = 0; j < NS; ++j)
             step(k0 + j, j);
-        }
     }
+#pragma unroll
+    for (int j = 0; j < NS - 1; ++j)
+        if (k0 + j < nin)
+            step(k0 + j, j);
 }
 
 int env_int(const char *name, int dflt)

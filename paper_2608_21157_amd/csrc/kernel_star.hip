@@ -72,7 +72,11 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
     constexpr int NQ = S::NQ, NH = S::NH;
     constexpr int E = sizeof(T);
     constexpr int RZ = ZAXIS ? R : 0;
-    __shared__ Vec16<T> lds_raw[S::NBUF][S::LDH * LDW / VEC];
+    // each LDS plane ends with 64 spare cells: a lane with no halo vector writes its
+    // lane's spare cell, so the writes (and the loads feeding them) need no branch; a
+    // load or store under a branch makes the compiler's wait counts conservative
+    constexpr int SPARE = S::LDH * LDW / VEC;
+    __shared__ Vec16<T> lds_raw[S::NBUF][SPARE + 64];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -110,7 +114,7 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
         own[o] = goff(gy, x);
         sto[o] = (gy < p.ny && x < p.nx) ? (gy * p.nx + x) * E : kOutOfRange;
     }
-    // halo vectors of this thread: global offset and LDS vector index (-1: none)
+    // halo vectors of this thread: global offset and LDS vector index (a spare cell: none)
     int hoff[NH], hlds[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
@@ -133,6 +137,8 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
         }
         if (hlds[h] >= 0)
             hoff[h] = goff(y0 + ly - R, x0 + lc - HX);
+        else
+            hlds[h] = SPARE + lane;
     }
 
     // weights: z by queue position (direction-aware), y and x by offset
@@ -178,19 +184,21 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
 
     Vec16<T> Q[NQ][TY];
     Vec16<T> hreg[NH];
-    // prologue: queue positions 0 .. 2R + PF hold planes zs + dir * (i - R); halo of zs
+    // prologue: halo of zs, then queue positions 0 .. 2R + PF (planes zs + dir * (i - R)).
+    // The halo goes first so that, at the loop head, as many loads follow it on the entry
+    // path as in the steady state: the wait before its LDS write then stays partial.
+    {
+        const auto rh = plane_rsrc(zs);
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+            hreg[h] = bload16<T>(rh, hoff[h]);
+    }
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
         const auto rq = plane_rsrc(zs + dir * (i - RZ));
 #pragma unroll
         for (int o = 0; o < TY; ++o)
             Q[i][o] = bload16<T>(rq, own[o]);
-    }
-    {
-        const auto rh = plane_rsrc(zs);
-#pragma unroll
-        for (int h = 0; h < NH; ++h)
-            hreg[h] = bload16<T>(rh, hoff[h]);
     }
 
     // one plane: iteration m (phase = m mod NQ) computes output plane zs + dir * m
@@ -203,13 +211,12 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
             buf[((R + strip + o) * LDW + HX + lxi * VEC) / VEC] = Q[(phase + RZ) % NQ][o];
 #pragma unroll
         for (int h = 0; h < NH; ++h)
-            if (hlds[h] >= 0)
-                buf[hlds[h]] = hreg[h];
-        if (ZAXIS && m + 1 < n) {
+            buf[hlds[h]] = hreg[h];
+        if (ZAXIS) {
             const auto rh = plane_rsrc(zc + dir);
 #pragma unroll
             for (int h = 0; h < NH; ++h)
-                hreg[h] = bload16<T>(rh, hoff[h]);
+                hreg[h] = bload16<T>(rh, m + 1 < n ? hoff[h] : kOutOfRange);
         }
         __syncthreads();
 
@@ -276,11 +283,11 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
         }
         // the slot of queue position 0 is free: prefetch plane zc + dir * (R + PF + 1),
         // which is first used PF + 1 planes from now
-        if (ZAXIS && m + PF + 1 <= n - 1) {
+        if (ZAXIS) {
             const auto rq = plane_rsrc(zc + dir * (R + PF + 1));
 #pragma unroll
             for (int o = 0; o < TY; ++o)
-                Q[phase][o] = bload16<T>(rq, own[o]);
+                Q[phase][o] = bload16<T>(rq, m + PF + 1 <= n - 1 ? own[o] : kOutOfRange);
         }
     };
 
@@ -288,14 +295,18 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
         step(0, 0);
         return;
     }
-    for (int m0 = 0; m0 < n; m0 += NQ) {
+    // whole groups of NQ planes in the loop, the remainder after it: an early exit inside
+    // the loop body would merge into the loop head and make its waits conservative
+    int m0 = 0;
+    for (; m0 + NQ <= n; m0 += NQ) {
 #pragma unroll
-        for (int ph = 0; ph < NQ; ++ph) {
-            if (m0 + ph >= n)
-                break;
+        for (int ph = 0; ph < NQ; ++ph)
             step(m0 + ph, ph);
-        }
     }
+#pragma unroll
+    for (int ph = 0; ph < NQ - 1; ++ph)
+        if (m0 + ph < n)
+            step(m0 + ph, ph);
 }
 
 int env_int(const char *name, int dflt)

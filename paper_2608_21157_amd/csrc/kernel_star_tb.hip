@@ -14,9 +14,9 @@
 //           blocks, which a star never reads, are skipped);
 //   stage 2 computes u2 on the tile, R planes behind stage 1.
 // One thread owns one column of the stage-1 region (a 16-byte vector along x): its u0
-// z-queue (2R + 1 planes plus one prefetched) and its u1 z-queue (2R + 1 planes) live in
-// registers.  Both queues rotate through the same 2R + 2 slots, so the loop is unrolled
-// 2R + 2 times and every register index is static.  The current u0 plane (stage 1's
+// z-queue (2R + 1 planes plus PF prefetched) and its u1 z-queue (2R + 1 planes) live in
+// registers.  Both queues rotate through the same 2R + 1 + PF slots, so the loop is
+// unrolled that many times and every register index is static.  The current u0 plane (stage 1's
 // in-plane neighbours, over the stage-1 region and one more band) and the current u1
 // plane (stage 2's in-plane neighbours) are staged in double-buffered LDS, one barrier
 // per plane.  Band threads use their u1 queue as the R-plane delay line that feeds the
@@ -38,7 +38,7 @@ struct Tb2Params {
     int channels;
 };
 
-template <typename T, int R>
+template <typename T, int R, int PF>
 struct Tb2Shape {
     static constexpr int VEC = Vec16<T>::N;
     static constexpr int TXV = 16;                       // tile width in vectors
@@ -60,7 +60,11 @@ struct Tb2Shape {
     // u1 over rows -R..TYW+R-1, vectors -HXV..TXV+HXV-1
     static constexpr int W0 = TXV + 4 * HXV, H0 = TYW + 4 * R;
     static constexpr int W1 = TXV + 2 * HXV, H1 = TYW + 2 * R;
-    static constexpr int NQ = 2 * R + 2;                 // queue slots (both queues)
+    // queue slots (both queues): the 2R + 1 planes of the window plus PF prefetched u0
+    // planes (PF odd, so that the slot count is even)
+    static constexpr int NQ = 2 * R + 1 + PF;
+    static_assert(NTILE % 64 == 0, "stage 2 must cover whole waves");
+    static_assert(NQ % 2 == 0, "the extra-cell registers alternate by iteration parity");
 };
 
 // LDS vector index of tile-relative (row r, vector v) in a rectangle whose origin is
@@ -70,17 +74,24 @@ __device__ __forceinline__ int rect_index(int r, int v, int oy, int ov, int w)
     return (r + oy) * w + (v + ov);
 }
 
-template <typename T, int R, bool PERIODIC, int STORE_CP>
-__global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_kernel(
+template <typename T, int R, int PF, bool PERIODIC, int STORE_CP>
+__global__ __launch_bounds__((Tb2Shape<T, R, PF>::THREADS)) void stencil_star_tb2_kernel(
     const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ w, Tb2Params p)
 {
-    using S = Tb2Shape<T, R>;
+    using S = Tb2Shape<T, R, PF>;
     constexpr int VEC = S::VEC, TXV = S::TXV, TYW = S::TYW, HXV = S::HXV, NQ = S::NQ;
     constexpr int E = sizeof(T);
-    __shared__ Vec16<T> lds0[2][S::H0 * S::W0];
-    __shared__ Vec16<T> lds1[2][S::H1 * S::W1];
+    // Each LDS plane ends with 64 spare cells: lanes that own no cell of a plane write
+    // their lane's spare cell instead, so every write is unconditional.  The loop body
+    // has no branch around a global load, store or LDS write; that keeps the compiler's
+    // wait counts exact, so a plane waits only for the loads it consumes and never for
+    // the store and prefetches just issued.
+    constexpr int SPARE0 = S::H0 * S::W0, SPARE1 = S::H1 * S::W1;
+    __shared__ Vec16<T> lds0[2][SPARE0 + 64];
+    __shared__ Vec16<T> lds1[2][SPARE1 + 64];
 
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
     int t = xcd_logical_block(blockIdx.x, p.nblocks);
     const int tx = t % p.ntx;
     t /= p.ntx;
@@ -95,7 +106,9 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     T *dst = out + b * p.vol;
 
     // ---- this thread's stage-1 column (tile-relative row r, vector v) ------------------
-    bool col = tid < S::NS1, tile = tid < S::NTILE;
+    // Lanes past the stage-1 columns (present when the column count is not a multiple of
+    // 64) compute on cell (0, 0), load nothing, store nothing and write spare cells.
+    const bool col = tid < S::NS1, tile = tid < S::NTILE;
     int r = 0, v = 0;
     if (tile) {
         r = tid / TXV;
@@ -114,7 +127,7 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
         }
     }
     const int gy = y0 + r, gx = x0 + v * VEC;
-    const bool inside = gy >= 0 && gy < p.ny && gx >= 0 && gx < p.nx;
+    const bool inside = col && gy >= 0 && gy < p.ny && gx >= 0 && gx < p.nx;
     auto goff = [&](int yy, int xx) {
         if (PERIODIC)
             return (wrap_index(yy, p.ny) * p.nx + wrap_index(xx, p.nx)) * E;
@@ -125,6 +138,8 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     const int soff = (tile && inside) ? (gy * p.nx + gx) * E : kOutOfRange;
     const int i0 = rect_index(r, v, 2 * R, 2 * HXV, S::W0);   // own cell in the u0 plane
     const int i1 = rect_index(r, v, R, HXV, S::W1);           // own cell in the u1 plane
+    const int w0 = col ? i0 : SPARE0 + lane;                  // where this lane writes
+    const int w1 = col ? i1 : SPARE1 + lane;
 
     // ---- u0 cells beyond the stage-1 columns that this thread stages ------------------
     int xoff[S::NEX], xidx[S::NEX];
@@ -132,29 +147,25 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     for (int h = 0; h < S::NEX; ++h) {
         int j = tid + h * S::THREADS;
         int rr = 0, vv = 0;
-        xidx[h] = -1;
-        xoff[h] = kOutOfRange;
+        bool any = true;
         if (j < S::NX_TB) {
             const int k = j / TXV;
             rr = k < R ? k - 2 * R : TYW + R + k - R;
             vv = j % TXV;
-            xidx[h] = 0;
         } else if ((j -= S::NX_TB) < S::NX_CORNER) {
             const int k = j % (2 * HXV);
             const int q = j / (2 * HXV);
             rr = q < R ? q - R : TYW + q - R;
             vv = k < HXV ? k - HXV : TXV + k - HXV;
-            xidx[h] = 0;
         } else if ((j -= S::NX_CORNER) < S::NX_LR) {
             const int k = j % (2 * HXV);
             rr = j / (2 * HXV);
             vv = k < HXV ? k - 2 * HXV : TXV + HXV + k - HXV;
-            xidx[h] = 0;
+        } else {
+            any = false;
         }
-        if (xidx[h] == 0) {
-            xidx[h] = rect_index(rr, vv, 2 * R, 2 * HXV, S::W0);
-            xoff[h] = goff(y0 + rr, x0 + vv * VEC);
-        }
+        xidx[h] = any ? rect_index(rr, vv, 2 * R, 2 * HXV, S::W0) : SPARE0 + lane;
+        xoff[h] = any ? goff(y0 + rr, x0 + vv * VEC) : kOutOfRange;
     }
 
     // ---- weights: z by queue position (direction-aware), y and x by offset -------------
@@ -180,6 +191,9 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     const int zs1 = dir > 0 ? z0 - R : z0 + n - 1 + R;  // stage-1 plane of iteration 0
     const int iters = n + 2 * R;
 
+    // A plane outside the grid gets a zero-length resource under the zero boundary (its
+    // loads return 0); periodic planes wrap.  Planes past the chunk's end are loaded
+    // harmlessly by the last iterations' prefetches.
     auto plane_rsrc = [&](int z) {
         bool ok = z >= 0 && z < p.nz;
         if (PERIODIC) {
@@ -191,21 +205,27 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     auto z_inside = [&](int z) { return PERIODIC || (z >= 0 && z < p.nz); };
 
     // ---- queues: position i of iteration m (phase m mod NQ) is slot (phase + i) mod NQ
-    // q0 position i holds u0 at plane z1 + dir * (i - R), i = 0 .. 2R + 1 (prefetch)
+    // q0 position i holds u0 at plane z1 + dir * (i - R), i = 0 .. 2R + PF (the last PF
+    // prefetched)
     // q1 position i holds u1 at plane z2 + dir * (i - R), i = 0 .. 2R, z2 = z1 - dir * R
-    Vec16<T> q0[NQ], q1[NQ], xr[S::NEX];
+    // xr[k] holds the extra cells of the plane of the next iteration with parity k (NQ is
+    // even, so the parity of the phase is the parity of the iteration)
+    // The extra cells are loaded before the queue so that, at the loop head, as many loads
+    // follow them on the entry path as in the steady state (the waits stay partial).
+    Vec16<T> q0[NQ], q1[NQ], xr[2][S::NEX];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const auto rx = plane_rsrc(zs1 + dir * k);
+#pragma unroll
+        for (int h = 0; h < S::NEX; ++h)
+            xr[k][h] = bload16<T>(rx, xoff[h]);
+    }
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
         q0[i] = bload16<T>(plane_rsrc(zs1 + dir * (i - R)), qoff);
 #pragma unroll
         for (int e = 0; e < VEC; ++e)
             q1[i].e[e] = T(0);
-    }
-    {
-        const auto rx = plane_rsrc(zs1);
-#pragma unroll
-        for (int h = 0; h < S::NEX; ++h)
-            xr[h] = bload16<T>(rx, xoff[h]);
     }
 
     // In-plane operands of one column: the 2R vectors above and below it and the HXV
@@ -275,60 +295,70 @@ __global__ __launch_bounds__((Tb2Shape<T, R>::THREADS)) void stencil_star_tb2_ke
     auto step = [&](int m, int phase) {
         const int z1 = zs1 + dir * m;
         const int z2 = z1 - dir * R;
-        Vec16<T> *b0 = lds0[phase & 1];
-        Vec16<T> *b1 = lds1[phase & 1];
-        // stage the u0 plane z1 (own columns and the extra cells) and the u1 plane z2
-        if (col) {
-            b0[i0] = q0[(phase + R) % NQ];
-            b1[i1] = q1[(phase + R) % NQ];
-        }
+        const int par = phase & 1;
+        Vec16<T> *b0 = lds0[par];
+        Vec16<T> *b1 = lds1[par];
+        // stage the u0 plane z1 (own columns and the extra cells) and the u1 plane z2,
+        // then refill the extra-cell registers with plane z1 + 2 dir
+        b0[w0] = q0[(phase + R) % NQ];
+        b1[w1] = q1[(phase + R) % NQ];
 #pragma unroll
         for (int h = 0; h < S::NEX; ++h)
-            if (xidx[h] >= 0)
-                b0[xidx[h]] = xr[h];
-        if (m + 1 < iters) {
-            const auto rx = plane_rsrc(z1 + dir);
+            b0[xidx[h]] = xr[par][h];
+        {
+            const auto rx = plane_rsrc(z1 + 2 * dir);
 #pragma unroll
             for (int h = 0; h < S::NEX; ++h)
-                xr[h] = bload16<T>(rx, xoff[h]);
+                xr[par][h] = bload16<T>(rx, xoff[h]);
         }
         __syncthreads();
 
-        if (col) {
-            // each stage reads its LDS operands together before its arithmetic (reading
-            // both stages' operands up front was measured slower: register pressure)
-            const bool st2 = tile && m >= 2 * R;
-            Vec16<T> g[NG];
-            gather(b0, i0, S::W0, g);
-            // stage 1: u1 at plane z1; zero outside the grid under the zero boundary
-            Vec16<T> u1 = stencil_at(g, q0, phase);
-            if (!PERIODIC && !(inside && z_inside(z1))) {
+        // stage 1: u1 at plane z1; zero outside the grid under the zero boundary
+        Vec16<T> g[NG];
+        gather(b0, i0, S::W0, g);
+        Vec16<T> u1 = stencil_at(g, q0, phase);
+        if (!PERIODIC) {
+            const bool keep = inside && z_inside(z1);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e)
-                    u1.e[e] = T(0);
-            }
-            q1[(phase + 2 * R) % NQ] = u1;
-            // stage 2: u2 at plane z2 (tile columns, once the u1 queue is full)
-            if (st2) {
-                gather(b1, i1, S::W1, g);
-                const Vec16<T> u2 = stencil_at(g, q1, phase);
-                bstore16<T, STORE_CP>(make_rsrc(dst + (long long)z2 * plane, plane_bytes),
-                                      soff, u2);
-            }
-            // queue position 0 is free: prefetch u0 at plane z1 + dir * (R + 2)
-            if (m + 2 < iters)
-                q0[phase] = bload16<T>(plane_rsrc(z1 + dir * (R + 2)), qoff);
+            for (int e = 0; e < VEC; ++e)
+                u1.e[e] = keep ? u1.e[e] : T(0);
         }
+        q1[(phase + 2 * R) % NQ] = u1;
+        // stage 2: u2 at plane z2 on the tile columns once the u1 queue is full (a
+        // wave-uniform condition: the tile is a whole number of waves).  Each stage reads
+        // its LDS operands together before its arithmetic; reading both stages' operands
+        // up front was measured slower (register pressure).
+        const bool st2 = tile && m >= 2 * R;
+        Vec16<T> u2;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            u2.e[e] = T(0);
+        if (st2) {
+            gather(b1, i1, S::W1, g);
+            u2 = stencil_at(g, q1, phase);
+        }
+        // the resource depends on the uniform iteration only (a per-lane base would make
+        // the compiler serialise the store over lanes); the offset masks the lanes
+        const bool full = m >= 2 * R;
+        bstore16<T, STORE_CP>(make_rsrc(dst + (long long)(full ? z2 : 0) * plane, plane_bytes),
+                              st2 ? soff : kOutOfRange, u2);
+        // queue position 0 is free: prefetch u0 at plane z1 + dir * (R + PF + 1), first
+        // used PF + 1 iterations from now
+        q0[phase] = bload16<T>(plane_rsrc(z1 + dir * (R + PF + 1)), qoff);
     };
 
-    for (int m0 = 0; m0 < iters; m0 += NQ) {
+    // whole groups of NQ iterations in the loop, the remainder after it: an early exit
+    // inside the loop body would merge into the loop head and make its waits conservative
+    int m0 = 0;
+    for (; m0 + NQ <= iters; m0 += NQ) {
 #pragma unroll
-        for (int ph = 0; ph < NQ; ++ph) {
-            if (m0 + ph >= iters)
-                break;
+        for (int ph = 0; ph < NQ; ++ph)
             step(m0 + ph, ph);
-        }
     }
+#pragma unroll
+    for (int ph = 0; ph < NQ - 1; ++ph)
+        if (m0 + ph < iters)
+            step(m0 + ph, ph);
 }
 
 int env_int(const char *name, int dflt)
@@ -337,10 +367,13 @@ int env_int(const char *name, int dflt)
     return (s && *s) ? std::atoi(s) : dflt;
 }
 
+// prefetched u0 planes per column
+constexpr int kPrefetch = 1;
+
 template <typename T, int R>
-Tb2Params make_params(const Geometry &g)
+Tb2Params make_params(const Geometry &g, int resident)
 {
-    using S = Tb2Shape<T, R>;
+    using S = Tb2Shape<T, R, kPrefetch>;
     Tb2Params p{};
     p.nz = int(g.nz);
     p.ny = int(g.ny);
@@ -350,9 +383,10 @@ Tb2Params make_params(const Geometry &g)
     p.nty = int((g.ny + S::TYW - 1) / S::TYW);
     p.channels = g.channels;
     const long long base = g.batch * p.ntx * p.nty;
-    // two workgroups per CU measured best; chunks of at least 8 radii so the 2R-plane
-    // start-up of stage 2 stays small
-    const long long target = env_int("STENCIL_TB_TARGET_BLOCKS", 512);
+    // one round of workgroups: as many as the GPU holds at once (measured best against
+    // 1.5x, 2x and 4x that: a second round runs with a ragged tail and more chunk starts);
+    // chunks of at least 8 radii so the 2R-plane start-up of stage 2 stays small
+    const long long target = env_int("STENCIL_TB_TARGET_BLOCKS", resident);
     long long nzc = (target + base - 1) / base;
     const long long min_len = 8 * R;
     const long long max_chunks = (p.nz + min_len - 1) / min_len;
@@ -366,22 +400,42 @@ Tb2Params make_params(const Geometry &g)
     return p;
 }
 
+// Workgroups of `kernel` the current device runs at once: resident blocks per CU (from
+// the kernel's registers and LDS) times the CU count.  Computed once per kernel; every
+// device the library drives is taken to be the same model.
+template <typename K>
+int resident_blocks(K kernel, int threads)
+{
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) !=
+            hipSuccess ||
+        cus < 1 || per_cu < 1)
+        return 256;
+    return cus * per_cu;
+}
+
+template <typename T, int R, bool PERIODIC, int CP>
+hipError_t launch_bc(const Geometry &g, const void *src, void *dst, const void *w,
+                     hipStream_t stream)
+{
+    using S = Tb2Shape<T, R, kPrefetch>;
+    const auto kernel = stencil_star_tb2_kernel<T, R, kPrefetch, PERIODIC, CP>;
+    static const int resident = resident_blocks(kernel, S::THREADS);
+    const Tb2Params p = make_params<T, R>(g, resident);
+    kernel<<<dim3(p.nblocks), dim3(S::THREADS), 0, stream>>>(
+        static_cast<const T *>(src), static_cast<T *>(dst), static_cast<const T *>(w), p);
+    return hipGetLastError();
+}
+
 template <typename T, int R, int CP>
 hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)
 {
-    using S = Tb2Shape<T, R>;
-    const Tb2Params p = make_params<T, R>(g);
-    const T *s = static_cast<const T *>(src);
-    T *d = static_cast<T *>(dst);
-    const T *wt = static_cast<const T *>(w);
     if (g.boundary == STENCIL_PERIODIC)
-        stencil_star_tb2_kernel<T, R, true, CP>
-            <<<dim3(p.nblocks), dim3(S::THREADS), 0, stream>>>(s, d, wt, p);
-    else
-        stencil_star_tb2_kernel<T, R, false, CP>
-            <<<dim3(p.nblocks), dim3(S::THREADS), 0, stream>>>(s, d, wt, p);
-    return hipGetLastError();
+        return launch_bc<T, R, true, CP>(g, src, dst, w, stream);
+    return launch_bc<T, R, false, CP>(g, src, dst, w, stream);
 }
 
 template <typename T, int R>

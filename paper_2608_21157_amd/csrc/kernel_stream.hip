@@ -17,13 +17,14 @@ int stream_max_depth(const Geometry &g)
 int stream_default_depth(const Geometry &g)
 {
     // Fusing two steps halves HBM traffic but costs redundant stage-1 work on the halo
-    // bands and LDS traffic that grow with the radius.  Measured on MI355X (512^3 and 256^3
-    // fp32): a clear win at radius 1, no gain at radius 4, where one step per launch is
-    // already close to the streaming-copy ceiling.
+    // bands and LDS traffic that grow with the radius.  Measured on MI355X, 4 steps per
+    // call, zero boundary, Gpoints/s at one step per launch -> two fused steps:
+    //   fp32 512^3:      R=1 643 -> 1205, R=2 617 -> 1005, R=3 598 -> 792, R=4 594 -> 699
+    //   fp64 256x512^2:  R=1 332 -> 631,  R=2 301 -> 500,  R=3 307 -> 387, R=4 311 -> 338
     // 2D boxes: two steps per pass measured 1.26x faster per step (10240^2 fp64, radius 3)
-    if (box2_tb2_supported(g))
+    if (box2_tb2_supported(g) || star_tb2_supported(g))
         return 2;
-    return (star_tb2_supported(g) && g.radius <= 2) ? 2 : 1;
+    return 1;
 }
 
 const char *stream_kernel_name(const Geometry &g, int depth)

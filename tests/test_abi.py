@@ -102,7 +102,9 @@ def test_forced_stream_variant_rejects_what_it_cannot_tile():
 def test_planner_choices():
     """The planner picks the tiled kernel family and temporal depth per description."""
     cases = [
-        (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=4), "stencil_star_stream_kernel", 1),
+        (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=4), "stencil_star_tb2_kernel", 2),
+        (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=4, temporal_depth=1),
+         "stencil_star_stream_kernel", 1),
         (B.make_desc(3, (256,) * 3, shape=B.STAR, radius=1), "stencil_star_tb2_kernel", 2),
         (B.make_desc(3, (512,) * 3, shape=B.BOX, radius=1, has_coeff_field=True,
                      boundary=B.PERIODIC), "stencil_box3_stream_kernel", 1),

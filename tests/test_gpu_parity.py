@@ -187,11 +187,11 @@ STAR_CASES = [(R, dt, bnd) for R in (1, 2, 3, 4) for dt in ("f32", "f64")
 @pytest.mark.parametrize("R,dt,bnd", STAR_CASES,
                          ids=["R%d-%s-%s" % (c[0], c[1], "zero" if c[2] == 0 else "per")
                               for c in STAR_CASES])
-@pytest.mark.parametrize("depth", [1, 0], ids=["depth1", "auto"])
+@pytest.mark.parametrize("depth", [1, 2, 0], ids=["depth1", "depth2", "auto"])
 def test_star_radius_dtype_boundary_depth(R, dt, bnd, depth):
-    """3D stars of every radius, fp32 and fp64, both boundaries, with steps fused two at
-    a time (auto) or one launch per step; ragged extents in every axis, 3 steps (one fused
-    pair plus a single step)."""
+    """3D stars of every radius, fp32 and fp64, both boundaries, one launch per step,
+    steps fused two at a time, or the planner's choice; ragged extents in every axis,
+    3 steps (one fused pair plus a single step)."""
     from dataclasses import replace
     g = np.random.default_rng(100 + R)
     dims = (23, 37, 72) if dt == "f32" else (21, 35, 40)
