@@ -211,6 +211,39 @@ def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
     return {"bytes": nbytes, "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}
 
 
+def tune_context(torch, B, head, K: int, W: int) -> dict:
+    """stencil_tune on the headline workload (a fresh plan of the same description, the
+    same buffers), then K calls of the tuned plan timed like the headline.  Context only:
+    the headline value is the planner's default plan."""
+    plan = B.Plan(head.plan.desc)
+    try:
+        rep = plan.tune(head.x, head.y, head.w, steps=head.wl.steps, field=head.k, reps=10,
+                        stream=head.stream)
+        info = plan.info()
+        for _ in range(W):
+            plan.run(head.x, head.y, head.w, steps=head.wl.steps, field=head.k,
+                     stream=head.stream)
+        head.stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(head.stream)
+        for _ in range(K):
+            plan.run(head.x, head.y, head.w, steps=head.wl.steps, field=head.k,
+                     stream=head.stream)
+        e1.record(head.stream)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1) / K
+    finally:
+        plan.close()
+    chosen = rep["candidates"][rep["chosen"]]
+    out = {"chosen": {k: chosen[k] for k in ("variant", "temporal_depth", "tile", "grid_scale")},
+           "kernel": info.kernel.decode(), "candidates": len(rep["candidates"]),
+           "valid": sum(c["valid"] for c in rep["candidates"]),
+           "tolerance": rep["tolerance"]}
+    out.update(figures(head.wl, ms))
+    return out
+
+
 def miopen_context(torch, wl, x_host, w, reps=5):
     """Time torch's convolution (MIOpen on ROCm) on the same workload, one stencil step per
     call: the MI355X counterpart of the paper's cuDNN dense reference.  Context only; its
@@ -277,6 +310,8 @@ def main() -> int:
                     help="override the workload's stencil steps per call (profiling runs)")
     ap.add_argument("--depth", type=int, default=0,
                     help="stencil steps fused per launch (0: the planner's choice)")
+    ap.add_argument("--no-tune", action="store_true",
+                    help="skip the stencil_tune context figure of the headline workload")
     ap.add_argument("--copy-only", action="store_true",
                     help="run only the copy probe (counter calibration runs)")
     args = ap.parse_args()
@@ -322,6 +357,11 @@ def main() -> int:
                 "algorithmic_bytes_per_launch": int(algo_per_launch)}
     log("[bench] %s: %.4f ms/call, %.1f Gpoints/s, %.1f GB/s (%.1f%% of 8 TB/s)" % (
         wl.name, ms, fig["gpoints_per_s"], achieved, 100 * achieved / HBM_PEAK_GBS))
+
+    tuned = None
+    if not args.no_tune:
+        tuned = tune_context(torch, B, head, args.steps, args.warmup)
+        log("[bench] tuned %s: %s" % (wl.name, tuned))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -379,6 +419,7 @@ def main() -> int:
                    "temporal_depth": head.depth, "parallelism": "single GPU"},
         "effective_gbs": fig["effective_gbs"],
         "roofline": roofline,
+        "tuned": tuned,
         "cpu_baseline": cpu,
         "copy_probe": probe,
         "workloads": others,

@@ -84,6 +84,17 @@ typedef struct {
     int32_t variant;         /* stencil_variant; 0 = AUTO */
     int32_t temporal_depth;  /* steps fused per launch where the variant supports it;
                                 0 = planner's choice, 1 = one launch per step */
+    int32_t tile;            /* workgroup tile of the one-step streaming kernels that have
+                                two: 0 = planner's choice, 1 = the smaller, 2 = the larger
+                                (3D star: 32- or 64-row x-y tiles; 3D box: 4 or 8 rows per
+                                lane).  The fused two-step kernels have one tile and ignore
+                                it.  Non-zero with a kernel family that has one tile, or with
+                                the generic variant: STENCIL_ERR_UNSUPPORTED */
+    int32_t grid_scale;      /* number of workgroups relative to the planner's choice, as a
+                                power of two, -2..2 (0 = planner's choice).  The streaming
+                                kernels split their streaming axis into correspondingly more
+                                or fewer chunks; the generic kernel caps its grid
+                                accordingly.  Results do not depend on it */
 } stencil_desc;
 
 typedef struct {
@@ -91,7 +102,30 @@ typedef struct {
     int32_t temporal_depth;  /* steps fused per launch */
     int64_t scratch_bytes;   /* device bytes the plan allocates for steps > 1 */
     const char *kernel;      /* base name of the dominant GPU kernel (static string) */
+    int32_t tile;            /* tile in use: 0 (the kernel has one), 1 or 2 */
+    int32_t grid_scale;      /* workgroup-count exponent in use */
 } stencil_plan_info;
+
+/* One candidate of stencil_tune(): a (variant, temporal depth, tile, grid scale) point. */
+typedef struct {
+    int32_t variant;         /* STENCIL_VARIANT_GENERIC or STENCIL_VARIANT_STREAM */
+    int32_t temporal_depth;
+    int32_t tile;
+    int32_t grid_scale;
+    int32_t valid;           /* 1: max_abs_err <= the tolerance (NaN is never valid) */
+    int32_t reserved;
+    double max_abs_err;      /* max over all points of |candidate - reference| */
+    double ms;               /* mean time of one call of `steps` steps; -1 if not timed */
+} stencil_tune_entry;
+
+#define STENCIL_TUNE_MAX_CANDIDATES 16
+
+typedef struct {
+    int32_t count;           /* candidates tried (entries filled) */
+    int32_t chosen;          /* index of the candidate fixed in the plan; -1 if none */
+    double tolerance;        /* the tolerance applied */
+    stencil_tune_entry entry[STENCIL_TUNE_MAX_CANDIDATES];
+} stencil_tune_report;
 
 /*
  * stencil_plan -- validate a description and create a plan for it.
@@ -129,6 +163,42 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
                              const int64_t dims[3], const void *coeffs,
                              const void *coeff_field, int32_t radius, int32_t boundary,
                              int32_t steps, hipStream_t stream);
+
+/*
+ * stencil_tune -- empirical plan-time search with a validity gate.  It mirrors the
+ * objective of HIERA (Sec. "Problem Formulation and Framework Overview", Eq. 2): the
+ * fastest candidate among those explored, subject to Valid(x) = 1.  Here the candidates
+ * are launch configurations of this library's kernels on the caller's own buffers.
+ *   Reference: the generic kernel (one thread per point, one launch per step) applied to
+ *     `in` for `steps` steps.
+ *   Candidates (at most STENCIL_TUNE_MAX_CANDIDATES): the generic kernel itself; then,
+ *     when the streaming variant can run the description and `in`, `out` and
+ *     `coeff_field` are 16-byte aligned, every supported temporal depth (1, 2) x every
+ *     tile of the one-step kernels (1, 2, or the single tile) x grid_scale in {-1, 0, 1}.
+ *   Validity: a candidate's `out` must satisfy max_p |out - reference| <= tolerance (on the
+ *     GPU, all points).  Invalid candidates are not timed.
+ *   Timing: one untimed call, then `reps` calls between HIP events on `stream`; mean.
+ *   Result: the fastest valid candidate is fixed in the plan (variant, depth, tile,
+ *     grid_scale; stencil_plan_query reports it), and `out` holds its result, i.e. `out`
+ *     receives u_steps exactly as stencil_apply() would.
+ * Arguments are those of stencil_apply() (same checks, same ownership), plus:
+ *   steps     : >= 1.
+ *   tolerance : < 0 selects c * steps * max(1, max|in|) with c = 2e-5 (f32) or 2e-12 (f64),
+ *               twice the per-step bound the library's tests hold each kernel to against
+ *               an fp64 evaluation; 0 accepts only results identical to the reference; a
+ *               positive value is an absolute bound.  Plans with a coefficient field whose
+ *               values exceed 1 in magnitude should pass their own bound.
+ *   reps      : timed calls per candidate, 1..1000 (0 selects 5).
+ *   report    : host pointer filled with every candidate, or NULL.
+ * Synchronous: returns after the stream has drained.  It allocates one grid-sized device
+ * buffer for the reference (freed before returning) and uses the plan's buffers.
+ * Returns STENCIL_OK, INVALID_ARG, MISMATCH, ALIAS, NO_MEMORY, UNSUPPORTED (no candidate
+ * passed the gate; the plan is left unchanged) or ERR_HIP.
+ */
+stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
+                            const int64_t dims[3], const void *coeffs, const void *coeff_field,
+                            int32_t steps, double tolerance, int32_t reps, hipStream_t stream,
+                            stencil_tune_report *report);
 
 /*
  * stencil_destroy -- free a plan and its device memory.  NULL is accepted.  The caller

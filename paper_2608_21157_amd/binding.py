@@ -25,7 +25,8 @@ VARIANT_AUTO, VARIANT_GENERIC, VARIANT_STREAM = 0, 1, 2
 VARIANT_NAMES = {VARIANT_GENERIC: "generic", VARIANT_STREAM: "stream"}
 
 EXPORTED = ("stencil_plan", "stencil_apply", "stencil_destroy", "stencil_plan_query",
-            "stencil_num_points", "stencil_status_str", "stencil_last_error")
+            "stencil_num_points", "stencil_status_str", "stencil_last_error", "stencil_tune")
+TUNE_MAX_CANDIDATES = 16
 
 
 class StencilDesc(ctypes.Structure):
@@ -34,12 +35,27 @@ class StencilDesc(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("shape", ctypes.c_int32),
                 ("radius", ctypes.c_int32), ("boundary", ctypes.c_int32),
                 ("has_coeff_field", ctypes.c_int32), ("variant", ctypes.c_int32),
-                ("temporal_depth", ctypes.c_int32)]
+                ("temporal_depth", ctypes.c_int32), ("tile", ctypes.c_int32),
+                ("grid_scale", ctypes.c_int32)]
 
 
 class StencilPlanInfo(ctypes.Structure):
     _fields_ = [("variant", ctypes.c_int32), ("temporal_depth", ctypes.c_int32),
-                ("scratch_bytes", ctypes.c_int64), ("kernel", ctypes.c_char_p)]
+                ("scratch_bytes", ctypes.c_int64), ("kernel", ctypes.c_char_p),
+                ("tile", ctypes.c_int32), ("grid_scale", ctypes.c_int32)]
+
+
+class StencilTuneEntry(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int32), ("temporal_depth", ctypes.c_int32),
+                ("tile", ctypes.c_int32), ("grid_scale", ctypes.c_int32),
+                ("valid", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("max_abs_err", ctypes.c_double), ("ms", ctypes.c_double)]
+
+
+class StencilTuneReport(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int32), ("chosen", ctypes.c_int32),
+                ("tolerance", ctypes.c_double),
+                ("entry", StencilTuneEntry * TUNE_MAX_CANDIDATES)]
 
 
 class StencilError(RuntimeError):
@@ -76,6 +92,10 @@ def load():
     lib.stencil_status_str.restype = ctypes.c_char_p
     lib.stencil_last_error.argtypes = []
     lib.stencil_last_error.restype = ctypes.c_char_p
+    lib.stencil_tune.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_int64), vp, vp,
+                                 ctypes.c_int32, ctypes.c_double, ctypes.c_int32, vp,
+                                 ctypes.POINTER(StencilTuneReport)]
+    lib.stencil_tune.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -101,6 +121,18 @@ def stencil_apply(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int 
     cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
     _check(load().stencil_apply(plan, inp, out, d, cp, coeff_field, radius, boundary, steps,
                                 stream))
+
+
+def stencil_tune(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int | None,
+                 steps: int, tolerance: float, reps: int, stream: int | None,
+                 report: StencilTuneReport | None = None) -> None:
+    """Arguments as ``stencil_apply`` plus the tolerance (< 0: the library's default),
+    the timed calls per candidate (0: 5) and an optional report to fill."""
+    d = (ctypes.c_int64 * 3)(*(list(dims) + [0] * (3 - len(dims))))
+    cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
+    rp = ctypes.byref(report) if report is not None else None
+    _check(load().stencil_tune(plan, inp, out, d, cp, coeff_field, steps, float(tolerance),
+                               reps, stream, rp))
 
 
 def stencil_destroy(plan: int | None) -> None:
@@ -129,7 +161,7 @@ def stencil_last_error() -> str:
 
 def make_desc(ndim, dims, *, batch=1, channels=1, dtype=F32, shape=STAR, radius=1,
               boundary=ZERO, has_coeff_field=False, variant=VARIANT_AUTO,
-              temporal_depth=0) -> StencilDesc:
+              temporal_depth=0, tile=0, grid_scale=0) -> StencilDesc:
     d = StencilDesc()
     d.ndim = ndim
     for i, v in enumerate(list(dims)[:3]):
@@ -137,6 +169,7 @@ def make_desc(ndim, dims, *, batch=1, channels=1, dtype=F32, shape=STAR, radius=
     d.batch, d.channels, d.dtype, d.shape = int(batch), int(channels), int(dtype), int(shape)
     d.radius, d.boundary, d.has_coeff_field = int(radius), int(boundary), int(bool(has_coeff_field))
     d.variant, d.temporal_depth = int(variant), int(temporal_depth)
+    d.tile, d.grid_scale = int(tile), int(grid_scale)
     return d
 
 
@@ -161,6 +194,27 @@ class Plan:
         stencil_apply(self.handle, x.data_ptr(), y.data_ptr(), self.dims, coeffs,
                       None if field is None else field.data_ptr(), self.desc.radius,
                       self.desc.boundary, steps, sh)
+
+    def tune(self, x, y, coeffs, *, steps: int, field=None, tolerance: float = -1.0,
+             reps: int = 0, stream=None) -> dict:
+        """``stencil_tune`` on torch tensors: fixes the fastest candidate that passes the
+        validity gate in this plan and leaves its result in ``y``.  Returns the report as
+        a dict: ``tolerance``, ``chosen`` (index) and ``candidates`` (list of dicts)."""
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        sh = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+        self._stream = stream
+        rep = StencilTuneReport()
+        stencil_tune(self.handle, x.data_ptr(), y.data_ptr(), self.dims, coeffs,
+                     None if field is None else field.data_ptr(), steps, tolerance, reps, sh,
+                     rep)
+        cands = [{"variant": VARIANT_NAMES.get(e.variant, str(e.variant)),
+                  "temporal_depth": e.temporal_depth, "tile": e.tile,
+                  "grid_scale": e.grid_scale, "valid": bool(e.valid),
+                  "max_abs_err": e.max_abs_err, "ms": e.ms}
+                 for e in rep.entry[: rep.count]]
+        return {"tolerance": rep.tolerance, "chosen": rep.chosen, "candidates": cands}
 
     def close(self) -> None:
         """Wait for the last stream this plan ran on, then free the plan."""

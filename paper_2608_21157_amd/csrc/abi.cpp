@@ -82,6 +82,11 @@ stencil_status validate_desc(const stencil_desc *d, Geometry *g)
         return fail(STENCIL_ERR_INVALID_ARG, "temporal_depth must be >= 0");
     if (d->variant < STENCIL_VARIANT_AUTO || d->variant > STENCIL_VARIANT_STREAM)
         return fail(STENCIL_ERR_INVALID_ARG, "unknown variant %d", d->variant);
+    if (d->tile < 0 || d->tile > 2)
+        return fail(STENCIL_ERR_INVALID_ARG, "tile must be 0, 1 or 2 (got %d)", d->tile);
+    if (d->grid_scale < -2 || d->grid_scale > 2)
+        return fail(STENCIL_ERR_INVALID_ARG, "grid_scale must be in -2..2 (got %d)",
+                    d->grid_scale);
     const int rmax = (d->shape == STENCIL_STAR) ? 4 : (d->ndim == 2 ? 4 : 3);
     if (d->radius > rmax)
         return fail(STENCIL_ERR_UNSUPPORTED, "radius %d exceeds %d for this shape", d->radius,
@@ -107,6 +112,8 @@ stencil_status validate_desc(const stencil_desc *d, Geometry *g)
     g->field = d->has_coeff_field != 0;
     g->dtype = d->dtype;
     g->elt = (d->dtype == STENCIL_F32) ? 4 : 8;
+    g->tile = d->tile;
+    g->grid_scale = d->grid_scale;
     return STENCIL_OK;
 }
 
@@ -119,6 +126,59 @@ bool overlaps(const void *a, const void *b, size_t bytes)
 bool aligned16(const void *p)
 {
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+// Host-side checks shared by stencil_apply and stencil_tune.
+stencil_status check_call(const Plan *p, const void *in, const void *out, const int64_t dims[3],
+                          const void *coeffs, const void *coeff_field, int32_t radius,
+                          int32_t boundary, int32_t steps)
+{
+    const Geometry &g = p->geo;
+    if (in == nullptr || out == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "in and out must be non-NULL device pointers");
+    if (coeffs == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "coeffs must be a host pointer");
+    if (dims == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "dims is NULL");
+    if (steps < 0)
+        return fail(STENCIL_ERR_INVALID_ARG, "steps must be >= 0 (got %d)", steps);
+    for (int a = 0; a < g.ndim; ++a)
+        if (dims[a] != p->desc.dims[a])
+            return fail(STENCIL_ERR_MISMATCH, "dims[%d] = %lld, plan has %lld", a,
+                        (long long)dims[a], (long long)p->desc.dims[a]);
+    if (radius != g.radius)
+        return fail(STENCIL_ERR_MISMATCH, "radius %d, plan has %d", radius, g.radius);
+    if (boundary != g.boundary)
+        return fail(STENCIL_ERR_MISMATCH, "boundary %d, plan has %d", boundary, g.boundary);
+    if ((coeff_field != nullptr) != g.field)
+        return fail(STENCIL_ERR_MISMATCH, g.field ? "the plan needs a coefficient field"
+                                                  : "the plan has no coefficient field");
+    const size_t bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
+    if (overlaps(in, out, bytes))
+        return fail(STENCIL_ERR_ALIAS, "out overlaps in");
+    if (coeff_field != nullptr && overlaps(coeff_field, out, bytes))
+        return fail(STENCIL_ERR_ALIAS, "out overlaps the coefficient field");
+    return STENCIL_OK;
+}
+
+// A launch configuration: what stencil_tune varies and fixes in the plan.
+struct Config {
+    int variant, depth, tile, grid_scale;
+};
+
+Config config_of(const Plan *p)
+{
+    return {p->variant, p->depth, p->geo.tile, p->geo.grid_scale};
+}
+
+void set_config(Plan *p, const Config &c)
+{
+    p->variant = c.variant;
+    p->depth = c.depth;
+    p->geo.tile = c.tile;
+    p->geo.grid_scale = c.grid_scale;
+    p->kernel = (c.variant == STENCIL_VARIANT_STREAM) ? stencil::stream_kernel_name(p->geo, c.depth)
+                                                      : "stencil_generic_kernel";
 }
 
 }  // namespace
@@ -173,6 +233,9 @@ stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan)
     if (depth > max_depth)
         return fail(STENCIL_ERR_UNSUPPORTED, "temporal_depth %d exceeds %d for this variant",
                     desc->temporal_depth, max_depth);
+    if (desc->tile != 0 && !(variant == STENCIL_VARIANT_STREAM && stencil::stream_has_tiles(g)))
+        return fail(STENCIL_ERR_UNSUPPORTED, "tile %d: this kernel family has a single tile",
+                    desc->tile);
 
     Plan *p = new (std::nothrow) Plan();
     if (p == nullptr)
@@ -198,6 +261,8 @@ stencil_status stencil_plan_query(stencil_plan_t plan, stencil_plan_info *info)
     info->temporal_depth = p->depth;
     info->scratch_bytes = int64_t(p->scratch_bytes);
     info->kernel = p->kernel;
+    info->tile = p->geo.tile;
+    info->grid_scale = p->geo.grid_scale;
     return STENCIL_OK;
 }
 
@@ -240,30 +305,11 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
         return fail(STENCIL_ERR_INVALID_ARG, "plan is NULL");
     Plan *p = reinterpret_cast<Plan *>(plan);
     const Geometry &g = p->geo;
-    if (in == nullptr || out == nullptr)
-        return fail(STENCIL_ERR_INVALID_ARG, "in and out must be non-NULL device pointers");
-    if (coeffs == nullptr)
-        return fail(STENCIL_ERR_INVALID_ARG, "coeffs must be a host pointer");
-    if (dims == nullptr)
-        return fail(STENCIL_ERR_INVALID_ARG, "dims is NULL");
-    if (steps < 0)
-        return fail(STENCIL_ERR_INVALID_ARG, "steps must be >= 0 (got %d)", steps);
-    for (int a = 0; a < g.ndim; ++a)
-        if (dims[a] != p->desc.dims[a])
-            return fail(STENCIL_ERR_MISMATCH, "dims[%d] = %lld, plan has %lld", a,
-                        (long long)dims[a], (long long)p->desc.dims[a]);
-    if (radius != g.radius)
-        return fail(STENCIL_ERR_MISMATCH, "radius %d, plan has %d", radius, g.radius);
-    if (boundary != g.boundary)
-        return fail(STENCIL_ERR_MISMATCH, "boundary %d, plan has %d", boundary, g.boundary);
-    if ((coeff_field != nullptr) != g.field)
-        return fail(STENCIL_ERR_MISMATCH, g.field ? "the plan needs a coefficient field"
-                                                  : "the plan has no coefficient field");
+    stencil_status st =
+        check_call(p, in, out, dims, coeffs, coeff_field, radius, boundary, steps);
+    if (st != STENCIL_OK)
+        return st;
     const size_t bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
-    if (overlaps(in, out, bytes))
-        return fail(STENCIL_ERR_ALIAS, "out overlaps in");
-    if (coeff_field != nullptr && overlaps(coeff_field, out, bytes))
-        return fail(STENCIL_ERR_ALIAS, "out overlaps the coefficient field");
 
     // fast kernels use 16-byte vector accesses; misaligned pointers run the generic kernel
     const bool fast = p->variant == STENCIL_VARIANT_STREAM && aligned16(in) && aligned16(out) &&
@@ -341,6 +387,181 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
         src = dst;
         left -= d;
     }
+    return STENCIL_OK;
+}
+
+stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
+                            const int64_t dims[3], const void *coeffs, const void *coeff_field,
+                            int32_t steps, double tolerance, int32_t reps, hipStream_t stream,
+                            stencil_tune_report *report)
+{
+    // ---- host-only validation (as stencil_apply, plus the tuning arguments) ----------
+    if (plan == nullptr)
+        return fail(STENCIL_ERR_INVALID_ARG, "plan is NULL");
+    Plan *p = reinterpret_cast<Plan *>(plan);
+    const Geometry &g = p->geo;
+    stencil_status st =
+        check_call(p, in, out, dims, coeffs, coeff_field, g.radius, g.boundary, steps);
+    if (st != STENCIL_OK)
+        return st;
+    if (steps < 1)
+        return fail(STENCIL_ERR_INVALID_ARG, "tuning needs steps >= 1 (got %d)", steps);
+    if (reps < 0 || reps > 1000)
+        return fail(STENCIL_ERR_INVALID_ARG, "reps must be in 0..1000 (got %d)", reps);
+    if (tolerance != tolerance)
+        return fail(STENCIL_ERR_INVALID_ARG, "tolerance is NaN");
+    if (reps == 0)
+        reps = 5;
+    if (report != nullptr) {
+        std::memset(report, 0, sizeof *report);
+        report->chosen = -1;
+    }
+
+    // ---- candidates: the reference first --------------------------------------------
+    Config cands[STENCIL_TUNE_MAX_CANDIDATES];
+    int nc = 0;
+    cands[nc++] = {STENCIL_VARIANT_GENERIC, 1, 0, 0};
+    const bool aligned = aligned16(in) && aligned16(out) &&
+                         (coeff_field == nullptr || aligned16(coeff_field));
+    if (aligned && stencil::stream_supported(g)) {
+        for (int depth = 1; depth <= stencil::stream_max_depth(g); ++depth) {
+            const bool tiles = depth == 1 && stencil::stream_has_tiles(g);
+            for (int tile = tiles ? 1 : 0; tile <= (tiles ? 2 : 0); ++tile)
+                for (int scale = -1; scale <= 1; ++scale)
+                    if (nc < STENCIL_TUNE_MAX_CANDIDATES)
+                        cands[nc++] = {STENCIL_VARIANT_STREAM, depth, tile, scale};
+        }
+    }
+
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (p->device >= 0 && dev != p->device)
+        return fail(STENCIL_ERR_MISMATCH, "plan belongs to device %d, current device is %d",
+                    p->device, dev);
+
+    const Config saved = config_of(p);
+    const int64_t n = g.batch * g.vol;
+    const size_t bytes = size_t(n) * g.elt;
+    void *ref = nullptr;
+    double *part = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    auto release = [&]() {
+        if (e0)
+            (void)hipEventDestroy(e0);
+        if (e1)
+            (void)hipEventDestroy(e1);
+        if (ref)
+            (void)hipFree(ref);
+        if (part)
+            (void)hipFree(part);
+    };
+    auto abort_with = [&](stencil_status s2) {
+        (void)hipStreamSynchronize(stream);
+        set_config(p, saved);
+        release();
+        return s2;
+    };
+    if ((e = hipMalloc(&ref, bytes)) != hipSuccess) {
+        ref = nullptr;
+        return abort_with(fail(e == hipErrorOutOfMemory ? STENCIL_ERR_NO_MEMORY : STENCIL_ERR_HIP,
+                               "hipMalloc(%zu) for the reference: %s", bytes,
+                               hipGetErrorString(e)));
+    }
+    if ((e = hipMalloc(&part, stencil::kCheckPartials * sizeof(double))) != hipSuccess) {
+        part = nullptr;
+        return abort_with(fail(e == hipErrorOutOfMemory ? STENCIL_ERR_NO_MEMORY : STENCIL_ERR_HIP,
+                               "hipMalloc for the check: %s", hipGetErrorString(e)));
+    }
+    if ((e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess)
+        return abort_with(hip_fail(e, "hipEventCreate"));
+    // max |a - b| (or max |a|) on the GPU, read back after the stream drains
+    auto max_abs = [&](const void *a, const void *b, double *result) -> stencil_status {
+        hipError_t e2 = stencil::launch_max_abs(g.dtype, a, b, n, part, stream);
+        if (e2 != hipSuccess)
+            return hip_fail(e2, "max-abs check launch");
+        if ((e2 = hipMemcpyAsync(result, part, sizeof(double), hipMemcpyDeviceToHost, stream)) !=
+                hipSuccess ||
+            (e2 = hipStreamSynchronize(stream)) != hipSuccess)
+            return hip_fail(e2, "max-abs check read-back");
+        return STENCIL_OK;
+    };
+    auto run = [&](const Config &c, void *dst) {
+        set_config(p, c);
+        return stencil_apply(plan, in, dst, dims, coeffs, coeff_field, g.radius, g.boundary,
+                             steps, stream);
+    };
+
+    // ---- reference and tolerance ---------------------------------------------------------
+    if ((st = run(cands[0], ref)) != STENCIL_OK)
+        return abort_with(st);
+    double tol = tolerance;
+    if (tol < 0) {
+        double in_max = 0.0;
+        if ((st = max_abs(in, nullptr, &in_max)) != STENCIL_OK)
+            return abort_with(st);
+        const double c = (g.dtype == STENCIL_F32) ? 2e-5 : 2e-12;
+        tol = c * double(steps) * (in_max > 1.0 ? in_max : 1.0);  // NaN input: NaN, no pass
+    }
+
+    // ---- every candidate: validity gate, then timing ---------------------------------
+    int best = -1, last = -1;
+    double best_ms = 0.0;
+    for (int i = 0; i < nc; ++i) {
+        if ((st = run(cands[i], out)) != STENCIL_OK)
+            return abort_with(st);
+        last = i;
+        double err = 0.0;
+        if ((st = max_abs(out, ref, &err)) != STENCIL_OK)
+            return abort_with(st);
+        const bool valid = err <= tol;  // false for NaN
+        double ms = -1.0;
+        if (valid) {
+            if ((e = hipEventRecord(e0, stream)) != hipSuccess)
+                return abort_with(hip_fail(e, "hipEventRecord"));
+            for (int r = 0; r < reps; ++r)
+                if ((st = run(cands[i], out)) != STENCIL_OK)
+                    return abort_with(st);
+            float total = 0.f;
+            if ((e = hipEventRecord(e1, stream)) != hipSuccess ||
+                (e = hipEventSynchronize(e1)) != hipSuccess ||
+                (e = hipEventElapsedTime(&total, e0, e1)) != hipSuccess)
+                return abort_with(hip_fail(e, "timing events"));
+            ms = double(total) / reps;
+            if (best < 0 || ms < best_ms) {
+                best = i;
+                best_ms = ms;
+            }
+        }
+        if (report != nullptr) {
+            stencil_tune_entry &r = report->entry[i];
+            r.variant = cands[i].variant;
+            r.temporal_depth = cands[i].depth;
+            r.tile = cands[i].tile;
+            r.grid_scale = cands[i].grid_scale;
+            r.valid = valid ? 1 : 0;
+            r.max_abs_err = err;
+            r.ms = ms;
+            report->count = i + 1;
+        }
+    }
+    if (report != nullptr)
+        report->tolerance = tol;
+    if (best < 0)
+        return abort_with(fail(STENCIL_ERR_UNSUPPORTED,
+                               "no candidate stayed within tolerance %g of the reference", tol));
+
+    // ---- fix the winner; leave its result in `out` --------------------------------------
+    if (best != last && (st = run(cands[best], out)) != STENCIL_OK)
+        return abort_with(st);
+    set_config(p, cands[best]);
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess)
+        return abort_with(hip_fail(e, "hipStreamSynchronize"));
+    release();
+    if (report != nullptr)
+        report->chosen = best;
+    g_last_error.clear();
     return STENCIL_OK;
 }
 

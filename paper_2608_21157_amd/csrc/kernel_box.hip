@@ -26,7 +26,6 @@
 #include "common.hpp"
 #include "plan.hpp"
 
-#include <cstdlib>
 
 namespace stencil {
 namespace {
@@ -252,12 +251,6 @@ int lanes_per_row(const Geometry &g, int vec)
     return (nxv >= 2 && 64 % nxv == 0) ? int(nxv) : 0;
 }
 
-int env_int(const char *name, int dflt)
-{
-    const char *s = std::getenv(name);
-    return (s && *s) ? std::atoi(s) : dflt;
-}
-
 template <typename T, int TY>
 BoxParams make_params(const Geometry &g)
 {
@@ -275,8 +268,9 @@ BoxParams make_params(const Geometry &g)
     p.ygroups = (p.ywaves + 3) / 4;
     p.channels = g.channels;
     const long long base = g.batch * p.segs * p.ygroups;
-    // enough workgroups to fill 256 CUs several times over; at least 8 planes per chunk
-    const long long target = env_int("STENCIL_BOX_TARGET_BLOCKS", 2048);
+    // enough workgroups to fill 256 CUs several times over (scaled by the plan's
+    // grid_scale); at least 8 planes per chunk
+    const long long target = scaled_target(2048, g.grid_scale);
     long long nzc = (target + base - 1) / base;
     const long long max_chunks = (p.nz + 7) / 8;
     if (nzc > max_chunks)
@@ -284,9 +278,6 @@ BoxParams make_params(const Geometry &g)
     if (nzc < 1)
         nzc = 1;
     p.zc = int((p.nz + nzc - 1) / nzc);
-    const int zc_env = env_int("STENCIL_BOX_ZC", 0);
-    if (zc_env > 0)
-        p.zc = zc_env < p.nz ? zc_env : p.nz;
     p.nzc = (p.nz + p.zc - 1) / p.zc;
     p.nblocks = int(base * p.nzc);
     return p;
@@ -341,9 +332,10 @@ hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, cons
                              const void *w, hipStream_t stream)
 {
     // measured on MI355X: 4-row blocks when a wavefront spans 64 lanes of one row,
-    // 8-row blocks when it spans several narrower rows
+    // 8-row blocks when it spans several narrower rows; the plan's tile forces 4 (tile 1)
+    // or 8 (tile 2)
     const int vec = (g.dtype == STENCIL_F32) ? 4 : 2;
-    const int ty = env_int("STENCIL_BOX_TY", lanes_per_row(g, vec) == 64 ? 4 : 8);
+    const int ty = g.tile == 1 ? 4 : g.tile == 2 ? 8 : (lanes_per_row(g, vec) == 64 ? 4 : 8);
     if (g.dtype == STENCIL_F32)
         return ty == 4 ? launch_ty<float, 4>(g, src, dst, field, w, stream)
                        : launch_ty<float, 8>(g, src, dst, field, w, stream);

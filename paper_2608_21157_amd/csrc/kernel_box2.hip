@@ -20,7 +20,6 @@
 #include "common.hpp"
 #include "plan.hpp"
 
-#include <cstdlib>
 
 namespace stencil {
 namespace {
@@ -450,12 +449,6 @@ __global__ __launch_bounds__(256) void stencil_box2_tb2_kernel(
             step(k0 + j, j);
 }
 
-int env_int(const char *name, int dflt)
-{
-    const char *s = std::getenv(name);
-    return (s && *s) ? std::atoi(s) : dflt;
-}
-
 int lanes_per_row(const Geometry &g, int vec)
 {
     if (g.nx % vec != 0)
@@ -482,7 +475,7 @@ Box2Params make_params(const Geometry &g)
     p.channels = g.channels;
     // about 16 wavefronts per CU in total; chunks of at least 16 radii of rows so the
     // 2R-row overlap between chunks stays small
-    const long long target = env_int("STENCIL_BOX2_TARGET_WAVES", 4096);
+    const long long target = scaled_target(4096, g.grid_scale);
     const long long per_image = g.batch * p.segs;
     long long rows_units = (target + per_image - 1) / per_image;  // row groups per image
     long long nchunks = rows_units;
@@ -516,7 +509,7 @@ Box2Params make_tb2_params(const Geometry &g)
     p.rg = 1;
     p.batch = g.batch;
     p.channels = g.channels;
-    const long long target = env_int("STENCIL_BOX2_TARGET_WAVES", 4096);
+    const long long target = scaled_target(4096, g.grid_scale);
     const long long per_image = g.batch * p.segs;
     long long nchunks = (target + per_image - 1) / per_image;
     const long long max_chunks = (p.ny + 32 * R - 1) / (32 * R);  // >= 32R rows per chunk

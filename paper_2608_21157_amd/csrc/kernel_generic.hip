@@ -93,8 +93,9 @@ hipError_t launch_t(const Geometry &g, const void *src, void *dst, const void *f
                     g.radius, g.channels};
     const int threads = 256;
     int64_t blocks = (p.total + threads - 1) / threads;
-    if (blocks > 65536)
-        blocks = 65536;
+    const int64_t cap = scaled_target(65536, g.grid_scale);  // grid-stride beyond the cap
+    if (blocks > cap)
+        blocks = cap;
     const T *s = static_cast<const T *>(src);
     T *d = static_cast<T *>(dst);
     const T *k = static_cast<const T *>(field);

@@ -23,7 +23,6 @@
 #include "common.hpp"
 #include "plan.hpp"
 
-#include <cstdlib>
 
 namespace stencil {
 namespace {
@@ -309,12 +308,6 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
             step(m0 + ph, ph);
 }
 
-int env_int(const char *name, int dflt)
-{
-    const char *s = std::getenv(name);
-    return (s && *s) ? std::atoi(s) : dflt;
-}
-
 template <typename T, int R, int TY, bool ZAXIS, int LX, int NW>
 StarParams make_params(const Geometry &g)
 {
@@ -330,8 +323,9 @@ StarParams make_params(const Geometry &g)
     const long long base = g.batch * p.ntx * p.nty;
     long long nzc = 1;
     if (ZAXIS) {
-        // enough workgroups for 256 CUs, with chunks of at least 4 queue depths
-        const long long target = env_int("STENCIL_STAR_TARGET_BLOCKS", 256);
+        // enough workgroups for 256 CUs (scaled by the plan's grid_scale), with chunks of
+        // at least 4 queue depths
+        const long long target = scaled_target(256, g.grid_scale);
         nzc = (target + base - 1) / base;
         const long long min_len = 4 * (2 * R + 1);
         const long long max_chunks = (p.nz + min_len - 1) / min_len;
@@ -341,9 +335,6 @@ StarParams make_params(const Geometry &g)
             nzc = 1;
     }
     p.zc = int((p.nz + nzc - 1) / nzc);
-    const int zc_env = env_int("STENCIL_STAR_ZC", 0);
-    if (ZAXIS && zc_env > 0)
-        p.zc = zc_env < p.nz ? zc_env : p.nz;
     p.nzc = (p.nz + p.zc - 1) / p.zc;
     p.nblocks = int(base * p.nzc);
     return p;
@@ -369,11 +360,13 @@ hipError_t launch_shape(const Geometry &g, const void *src, void *dst, const voi
 // Tile shape, measured on MI355X (512^3, radius 4): 64 x 64 tiles (8 wavefronts) with one
 // prefetched plane were the fastest of the 16/32/64-lane-wide, 4/8-wavefront and 1/3/5-plane
 // prefetch variants (all within a few percent); 2D grids use 64 x 32 tiles for more tiles.
+// The plan's tile selects 64 x 32 (tile 1) or 64 x 64 (tile 2) explicitly.
 template <typename T, int R, int TY, bool ZAXIS, int CP>
 hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)
 {
-    if (ZAXIS)
+    const bool large = g.tile == 2 || (g.tile == 0 && ZAXIS);
+    if (large)
         return launch_shape<T, R, TY, ZAXIS, CP, 16, 8, 1>(g, src, dst, w, stream);
     return launch_shape<T, R, TY, ZAXIS, CP, 16, 4, 1>(g, src, dst, w, stream);
 }

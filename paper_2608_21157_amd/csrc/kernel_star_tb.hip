@@ -24,7 +24,6 @@
 #include "common.hpp"
 #include "plan.hpp"
 
-#include <cstdlib>
 
 namespace stencil {
 namespace {
@@ -361,12 +360,6 @@ __global__ __launch_bounds__((Tb2Shape<T, R, PF>::THREADS)) void stencil_star_tb
             step(m0 + ph, ph);
 }
 
-int env_int(const char *name, int dflt)
-{
-    const char *s = std::getenv(name);
-    return (s && *s) ? std::atoi(s) : dflt;
-}
-
 // prefetched u0 planes per column
 constexpr int kPrefetch = 1;
 
@@ -386,7 +379,7 @@ Tb2Params make_params(const Geometry &g, int resident)
     // one round of workgroups: as many as the GPU holds at once (measured best against
     // 1.5x, 2x and 4x that: a second round runs with a ragged tail and more chunk starts);
     // chunks of at least 8 radii so the 2R-plane start-up of stage 2 stays small
-    const long long target = env_int("STENCIL_TB_TARGET_BLOCKS", resident);
+    const long long target = scaled_target(resident, g.grid_scale);
     long long nzc = (target + base - 1) / base;
     const long long min_len = 8 * R;
     const long long max_chunks = (p.nz + min_len - 1) / min_len;

@@ -27,6 +27,12 @@ int stream_default_depth(const Geometry &g)
     return 1;
 }
 
+bool stream_has_tiles(const Geometry &g)
+{
+    // box3: 4 or 8 rows per lane; star (one step): 32- or 64-row workgroup tiles
+    return box_stream_supported(g) || star_stream_supported(g);
+}
+
 const char *stream_kernel_name(const Geometry &g, int depth)
 {
     if (box_stream_supported(g))

@@ -25,11 +25,20 @@ struct Geometry {
     bool field;
     int dtype;        // STENCIL_F32 / STENCIL_F64
     size_t elt;       // bytes per element
+    int tile;         // one-step streaming tile: 0 = default, 1 = smaller, 2 = larger
+    int grid_scale;   // workgroup count relative to the default, as a power of two
 };
+
+// A kernel's default workgroup (or wavefront) count scaled by 2^grid_scale, at least 1.
+inline long long scaled_target(long long dflt, int grid_scale)
+{
+    long long t = grid_scale >= 0 ? dflt << grid_scale : dflt >> -grid_scale;
+    return t < 1 ? 1 : t;
+}
 
 struct Plan {
     stencil_desc desc{};
-    Geometry geo{};
+    Geometry geo{};                // geo.tile and geo.grid_scale hold the launch choice
     int variant = STENCIL_VARIANT_GENERIC;
     int depth = 1;                 // steps fused per launch
     const char *kernel = "";
@@ -77,6 +86,16 @@ hipError_t launch_box2_stream(const Geometry &g, const void *src, void *dst, con
 bool star_tb2_supported(const Geometry &g);
 hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,
                            hipStream_t stream);
+
+// Whether the one-step streaming kernel of this geometry offers two tiles (tile 1 / 2).
+bool stream_has_tiles(const Geometry &g);
+
+// max |a - b| over n elements of the given dtype (max |a| when b is NULL), computed on the
+// GPU.  `partial` is device memory for kCheckPartials doubles; the result lands in
+// partial[0] (NaN if any difference is NaN).
+constexpr int kCheckPartials = 1025;
+hipError_t launch_max_abs(int dtype, const void *a, const void *b, int64_t n, double *partial,
+                          hipStream_t stream);
 
 // 2.5D z-streaming kernels.  `supported` says whether the kernel family can run a
 // geometry (shape, radius, alignment of the x extent); launch_* run one pass.

@@ -26,7 +26,7 @@ def tolerance(wl, x, k=None, steps=None) -> float:
 
 
 def run_library(wl, x, w, k=None, *, steps=None, variant=B.VARIANT_AUTO, depth=0,
-                stream=None):
+                stream=None, tile=0, grid_scale=0):
     """Upload, apply through the C ABI, download.  Returns (result float64, plan info)."""
     steps = wl.steps if steps is None else steps
     dev = torch.device("cuda:0")
@@ -38,12 +38,13 @@ def run_library(wl, x, w, k=None, *, steps=None, variant=B.VARIANT_AUTO, depth=0
     desc = B.make_desc(wl.ndim, xt.shape[xt.dim() - wl.ndim:], batch=batch,
                        channels=wl.channels, dtype=B.F32 if wl.dtype == "f32" else B.F64,
                        shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
-                       has_coeff_field=k is not None, variant=variant, temporal_depth=depth)
+                       has_coeff_field=k is not None, variant=variant, temporal_depth=depth,
+                       tile=tile, grid_scale=grid_scale)
     plan = B.Plan(desc)
     try:
         info = plan.info()
         info = dict(variant=info.variant, depth=info.temporal_depth,
-                    kernel=info.kernel.decode())
+                    kernel=info.kernel.decode(), tile=info.tile, grid_scale=info.grid_scale)
         plan.run(xt, yt, w, steps=steps, field=kt, stream=stream)
         torch.cuda.synchronize()
     finally:

@@ -73,6 +73,12 @@ def test_status_strings_and_point_counts():
     (dict(temporal_depth=-1), B.ERR_INVALID_ARG),
     (dict(variant=B.VARIANT_GENERIC, temporal_depth=2), B.ERR_UNSUPPORTED),
     (dict(dims=(1 << 11, 1 << 11, 1 << 11)), B.ERR_UNSUPPORTED),
+    (dict(tile=3), B.ERR_INVALID_ARG),
+    (dict(tile=-1), B.ERR_INVALID_ARG),
+    (dict(grid_scale=3), B.ERR_INVALID_ARG),
+    (dict(grid_scale=-3), B.ERR_INVALID_ARG),
+    (dict(variant=B.VARIANT_GENERIC, tile=1), B.ERR_UNSUPPORTED),
+    (dict(dims=(8, 8, 10), tile=2), B.ERR_UNSUPPORTED),          # generic only (x % 4)
 ])
 def test_plan_rejects(kw, status):
     assert status_of(B.stencil_plan, desc3(**kw)) == status
@@ -136,6 +142,21 @@ def test_plan_and_query_without_gpu():
     B.stencil_destroy(None)
 
 
+def test_tile_and_grid_scale_choices():
+    """tile is accepted where the one-step kernel has two (3D star, 3D box), refused for the
+    2D box family; grid_scale is accepted by every variant; the plan reports both."""
+    for d, tile in ((desc3(dims=(64, 64, 256), radius=4, tile=1, grid_scale=-2), 1),
+                    (desc3(dims=(64, 64, 256), shape=B.BOX, tile=2, grid_scale=2), 2),
+                    (desc3(dims=(8, 8, 10), grid_scale=1), 0)):
+        h = B.stencil_plan(d)
+        info = B.stencil_plan_query(h)
+        assert (info.tile, info.grid_scale) == (tile, d.grid_scale)
+        B.stencil_destroy(h)
+    box2 = B.make_desc(2, (1024, 1024), shape=B.BOX, radius=3, dtype=B.F64, tile=1)
+    assert status_of(B.stencil_plan, box2) == B.ERR_UNSUPPORTED
+    assert "single tile" in B.stencil_last_error()
+
+
 @pytest.fixture
 def plan():
     h = B.stencil_plan(desc3(dims=(4, 5, 6), shape=B.BOX, radius=1, has_coeff_field=True))
@@ -188,4 +209,40 @@ def test_valid_apply_without_gpu_reports_hip_error(plan):
     if torch.cuda.is_available():
         pytest.skip("a GPU is present")
     assert apply_status(plan) == B.ERR_HIP
+    assert "hipGetDevice" in B.stencil_last_error()
+
+
+def tune_status(h, inp=IN, out=OUT, dims=(4, 5, 6), coeffs=W27, field=FIELD, steps=1,
+                tolerance=-1.0, reps=0, report=None):
+    return status_of(B.stencil_tune, h, inp, out, dims, coeffs, field, steps, tolerance, reps,
+                     None, report)
+
+
+def test_tune_validation(plan):
+    """stencil_tune checks everything stencil_apply checks, plus its own arguments, on the
+    host; a failed call leaves the report untouched and the plan unchanged."""
+    rep = B.StencilTuneReport()
+    rep.count = 77
+    assert tune_status(None) == B.ERR_INVALID_ARG
+    assert tune_status(plan, inp=None, report=rep) == B.ERR_INVALID_ARG
+    assert tune_status(plan, coeffs=None) == B.ERR_INVALID_ARG
+    assert tune_status(plan, dims=(4, 5, 7)) == B.ERR_MISMATCH
+    assert tune_status(plan, field=None) == B.ERR_MISMATCH
+    assert tune_status(plan, out=IN + 8) == B.ERR_ALIAS
+    assert tune_status(plan, steps=0) == B.ERR_INVALID_ARG
+    assert "steps >= 1" in B.stencil_last_error()
+    assert tune_status(plan, reps=-1) == B.ERR_INVALID_ARG
+    assert tune_status(plan, reps=1001) == B.ERR_INVALID_ARG
+    assert tune_status(plan, tolerance=float("nan")) == B.ERR_INVALID_ARG
+    assert rep.count == 77
+    info = B.stencil_plan_query(plan)
+    assert (info.variant, info.temporal_depth, info.tile, info.grid_scale) == (
+        B.VARIANT_STREAM, 1, 0, 0) or info.variant == B.VARIANT_GENERIC
+
+
+def test_valid_tune_without_gpu_reports_hip_error(plan):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert tune_status(plan, steps=2) == B.ERR_HIP
     assert "hipGetDevice" in B.stencil_last_error()
