@@ -54,6 +54,24 @@ __device__ __forceinline__ double dpp_move(double src, double old)
                                 static_cast<unsigned int>(lo));
 }
 
+// DPP move whose lanes without a source (lane 0 for wave_shr, lane 63 for wave_shl)
+// receive zero (bound_ctrl), so no destination initialisation is needed.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move_zero(float src)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(src), CTRL, 0xF, 0xF, true));
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_move_zero(double src)
+{
+    const long long s = __double_as_longlong(src);
+    const int lo = __builtin_amdgcn_mov_dpp(int(s), CTRL, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp(int(s >> 32), CTRL, 0xF, 0xF, true);
+    return __longlong_as_double((static_cast<long long>(hi) << 32) |
+                                static_cast<unsigned int>(lo));
+}
+
 // Value of lane - 1 (lane 0 receives `old`).
 template <typename T>
 __device__ __forceinline__ T from_left_lane(T v, T old)
@@ -66,6 +84,19 @@ template <typename T>
 __device__ __forceinline__ T from_right_lane(T v, T old)
 {
     return dpp_move<kDppWaveShl1>(v, old);
+}
+
+// Value of lane - 1 (lane 0 receives 0) and of lane + 1 (lane 63 receives 0).
+template <typename T>
+__device__ __forceinline__ T from_left_lane_or_zero(T v)
+{
+    return dpp_move_zero<kDppWaveShr1>(v);
+}
+
+template <typename T>
+__device__ __forceinline__ T from_right_lane_or_zero(T v)
+{
+    return dpp_move_zero<kDppWaveShl1>(v);
 }
 
 // Raw buffer access (gfx9 resource word 3 = 0x00020000, stride 0).  Offsets are byte
