@@ -468,8 +468,20 @@ int lanes_per_row(const Geometry &g, int vec)
     return (nxv >= 2 && 64 % nxv == 0) ? int(nxv) : 0;
 }
 
+// Wavefront count of a launch: at most one round of the waves the GPU holds at once
+// (`resident`, scaled by the plan's grid_scale), in whole chunks per image.  A second,
+// partly filled round left the GPU idle for most of its length: on 10240^2 fp64, radius 3,
+// 4128 waves against 3072 resident ran 1.34 rounds.
+inline long long whole_chunks(long long target, long long per_image, long long max_chunks)
+{
+    long long nchunks = target / per_image;
+    if (nchunks > max_chunks)
+        nchunks = max_chunks;
+    return nchunks < 1 ? 1 : nchunks;
+}
+
 template <typename T, int R>
-Box2Params make_params(const Geometry &g)
+Box2Params make_params(const Geometry &g, int resident_waves)
 {
     constexpr int VEC = Vec16<T>::N;
     Box2Params p{};
@@ -482,18 +494,13 @@ Box2Params make_params(const Geometry &g)
     p.rg = 64 / p.lpr;
     p.batch = g.batch;
     p.channels = g.channels;
-    // about 16 wavefronts per CU in total; chunks of at least 16 radii of rows so the
-    // 2R-row overlap between chunks stays small
-    const long long target = scaled_target(4096, g.grid_scale);
+    // one round of wavefronts; chunks of at least 16 radii of rows so the 2R-row overlap
+    // between chunks stays small
+    const long long target = scaled_target(resident_waves, g.grid_scale);
     const long long per_image = g.batch * p.segs;
-    long long rows_units = (target + per_image - 1) / per_image;  // row groups per image
-    long long nchunks = rows_units;
     const long long min_len = 16 * R;
-    const long long max_chunks = (p.ny + min_len - 1) / min_len;
-    if (nchunks > max_chunks)
-        nchunks = max_chunks;
-    if (nchunks < 1)
-        nchunks = 1;
+    const long long nchunks =
+        whole_chunks(target * p.rg, per_image, (p.ny + min_len - 1) / min_len);
     // chunks are taken rg at a time by a wavefront
     long long total = ((nchunks + p.rg - 1) / p.rg) * p.rg;
     p.yc = int((p.ny + total - 1) / total);
@@ -504,7 +511,7 @@ Box2Params make_params(const Geometry &g)
 }
 
 template <typename T, int R>
-Box2Params make_tb2_params(const Geometry &g)
+Box2Params make_tb2_params(const Geometry &g, int resident_waves)
 {
     constexpr int VEC = Vec16<T>::N;
     constexpr int HXV = (R + VEC - 1) / VEC;
@@ -518,14 +525,10 @@ Box2Params make_tb2_params(const Geometry &g)
     p.rg = 1;
     p.batch = g.batch;
     p.channels = g.channels;
-    const long long target = scaled_target(4096, g.grid_scale);
+    const long long target = scaled_target(resident_waves, g.grid_scale);
     const long long per_image = g.batch * p.segs;
-    long long nchunks = (target + per_image - 1) / per_image;
-    const long long max_chunks = (p.ny + 32 * R - 1) / (32 * R);  // >= 32R rows per chunk
-    if (nchunks > max_chunks)
-        nchunks = max_chunks;
-    if (nchunks < 1)
-        nchunks = 1;
+    const long long nchunks =  // >= 32R rows per chunk
+        whole_chunks(target, per_image, (p.ny + 32 * R - 1) / (32 * R));
     p.yc = int((p.ny + nchunks - 1) / nchunks);
     p.nyc = (p.ny + p.yc - 1) / p.yc;
     const long long waves = g.batch * p.segs * p.nyc;
@@ -537,16 +540,20 @@ template <typename T, int R, int CP>
 hipError_t launch_tb2_cp(const Geometry &g, const void *src, void *dst, const void *w,
                          hipStream_t stream)
 {
-    const Box2Params p = make_tb2_params<T, R>(g);
     const T *s = static_cast<const T *>(src);
     T *d = static_cast<T *>(dst);
     const T *wt = static_cast<const T *>(w);
-    if (g.boundary == STENCIL_PERIODIC)
-        stencil_box2_tb2_kernel<T, R, true, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
-    else
-        stencil_box2_tb2_kernel<T, R, false, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    if (g.boundary == STENCIL_PERIODIC) {
+        const auto k = stencil_box2_tb2_kernel<T, R, true, CP>;
+        static const int resident = 4 * resident_blocks(k, 256);
+        const Box2Params p = make_tb2_params<T, R>(g, resident);
+        k<<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    } else {
+        const auto k = stencil_box2_tb2_kernel<T, R, false, CP>;
+        static const int resident = 4 * resident_blocks(k, 256);
+        const Box2Params p = make_tb2_params<T, R>(g, resident);
+        k<<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    }
     return hipGetLastError();
 }
 
@@ -554,16 +561,20 @@ template <typename T, int R, int CP>
 hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)
 {
-    const Box2Params p = make_params<T, R>(g);
     const T *s = static_cast<const T *>(src);
     T *d = static_cast<T *>(dst);
     const T *wt = static_cast<const T *>(w);
-    if (g.boundary == STENCIL_PERIODIC)
-        stencil_box2_stream_kernel<T, R, true, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
-    else
-        stencil_box2_stream_kernel<T, R, false, CP>
-            <<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    if (g.boundary == STENCIL_PERIODIC) {
+        const auto k = stencil_box2_stream_kernel<T, R, true, CP>;
+        static const int resident = 4 * resident_blocks(k, 256);
+        const Box2Params p = make_params<T, R>(g, resident);
+        k<<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    } else {
+        const auto k = stencil_box2_stream_kernel<T, R, false, CP>;
+        static const int resident = 4 * resident_blocks(k, 256);
+        const Box2Params p = make_params<T, R>(g, resident);
+        k<<<dim3(p.nblocks), dim3(256), 0, stream>>>(s, d, wt, p);
+    }
     return hipGetLastError();
 }
 

@@ -393,22 +393,6 @@ Tb2Params make_params(const Geometry &g, int resident)
     return p;
 }
 
-// Workgroups of `kernel` the current device runs at once: resident blocks per CU (from
-// the kernel's registers and LDS) times the CU count.  Computed once per kernel; every
-// device the library drives is taken to be the same model.
-template <typename K>
-int resident_blocks(K kernel, int threads)
-{
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) !=
-            hipSuccess ||
-        cus < 1 || per_cu < 1)
-        return 256;
-    return cus * per_cu;
-}
-
 template <typename T, int R, bool PERIODIC, int CP>
 hipError_t launch_bc(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)

@@ -36,6 +36,23 @@ inline long long scaled_target(long long dflt, int grid_scale)
     return t < 1 ? 1 : t;
 }
 
+// Workgroups of `kernel` the current device runs at once: resident blocks per CU (from
+// the kernel's registers and LDS, through the HIP occupancy API) times the CU count; 256
+// if the query fails.  Launchers call it once per kernel (a function-local static): every
+// device the library drives is taken to be the same model.
+template <typename K>
+int resident_blocks(K kernel, int threads)
+{
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) !=
+            hipSuccess ||
+        cus < 1 || per_cu < 1)
+        return 256;
+    return cus * per_cu;
+}
+
 struct Plan {
     stencil_desc desc{};
     Geometry geo{};                // geo.tile and geo.grid_scale hold the launch choice
