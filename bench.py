@@ -36,12 +36,12 @@ PAPER_STEPS_TIMED = 256
 PAPER_A100_MS_PER_STEP = {"best_generated_kernel": 4.71, "cudnn_implicit_precomp_gemm": 7.23}
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
-    "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp"],
-    "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp"],
-    "stencil_star_tb2_kernel": ["kernel_star_tb.hip", "common.hpp"],
-    "stencil_box2_stream_kernel": ["kernel_box2.hip", "common.hpp"],
-    "stencil_box2_tb2_kernel": ["kernel_box2.hip", "common.hpp"],
-    "stencil_generic_kernel": ["kernel_generic.hip"],
+    "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp", "plan.hpp"],
+    "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp", "plan.hpp"],
+    "stencil_star_tb2_kernel": ["kernel_star_tb.hip", "common.hpp", "plan.hpp"],
+    "stencil_box2_stream_kernel": ["kernel_box2.hip", "common.hpp", "plan.hpp"],
+    "stencil_box2_tb2_kernel": ["kernel_box2.hip", "common.hpp", "plan.hpp"],
+    "stencil_generic_kernel": ["kernel_generic.hip", "plan.hpp"],
 }
 
 
