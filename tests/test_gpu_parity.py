@@ -259,3 +259,36 @@ def test_paper_workload_full_size_sampled():
                               steps=wl.steps, ndim=2)
     report("paper full (%d samples)" % len(pts), gather(got, pts, wl), ref, tolerance(wl, x))
     assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("depth", [2, 1], ids=["fused", "one-step"])
+def test_maximum_size_star_1024_cubed(depth):
+    """The largest grid the tests drive: 1024^3 fp32 (2^30 points, 4 GiB per grid, eight
+    times the headline volume), the 25-point radius-4 star over 2 steps, fused or one step
+    per launch.  Results are gathered on the GPU at sampled points (every corner, points
+    near the faces, random interior points) and compared with the oracle there."""
+    dims = (1024, 1024, 1024)
+    wl = WORKLOADS["c3"].resized(dims, steps=2)
+    _, w, _ = inputs.make(WORKLOADS["c3"].resized((8, 8, 8)))  # the c3 weights
+    g = np.random.default_rng(77)
+    x = g.random(dims, dtype=np.float32)
+    x *= 2
+    x -= 1
+    print("[case] max size %s depth=%d" % (dims, depth), flush=True)
+    xt = torch.from_numpy(x).to("cuda:0")
+    yt = torch.empty_like(xt)
+    plan = B.Plan(B.make_desc(3, dims, shape=B.STAR, radius=4, temporal_depth=depth))
+    try:
+        assert plan.info().temporal_depth == depth
+        plan.run(xt, yt, w, steps=wl.steps)
+        torch.cuda.synchronize()
+    finally:
+        plan.close()
+    pts = sample_points(wl, x, 300, seed=5)
+    idx = torch.from_numpy(pts).to("cuda:0")
+    got = yt[idx[:, 1], idx[:, 2], idx[:, 3]].double().cpu().numpy()
+    assert bool(torch.isfinite(yt).all())
+    del xt, yt
+    ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius,
+                              boundary=wl.boundary, steps=wl.steps)
+    report("max size depth %d (%d samples)" % (depth, len(pts)), got, ref, tolerance(wl, x))
