@@ -25,6 +25,8 @@ import statistics
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -280,20 +282,51 @@ def miopen_context(torch, wl, x_host, w, reps=5):
         return {"error": str(e)[:200]}
 
 
-def cpu_baseline(wl, x_host, w, planes: int):
-    """The fp64 oracle, single-threaded, on a z-slab of the headline input."""
+def host_info(torch) -> dict:
+    """CPU model, logical CPUs, ROCm and torch versions of the measuring host."""
+    info = {"cpus": os.cpu_count(), "torch": torch.__version__}
+    try:
+        with open("/proc/cpuinfo") as f:
+            info["cpu"] = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            info["rocm"] = f.read().strip()
+    except OSError:
+        pass
+    try:
+        info["gpu"] = torch.cuda.get_device_name(0)
+    except Exception:
+        pass
+    return info
+
+
+def cpu_baseline(wl, x_host, w, planes: int, y_gpu=None):
+    """The fp64 oracle, single-threaded, on a z-slab of the headline input.  With the
+    GPU's result `y_gpu` (the same leading planes, zero boundary), the slab's planes
+    below z = planes - R * steps -- those the cut face cannot reach in `steps` steps --
+    are also compared with it point by point."""
     import oracle
     oracle.build()
     slab = x_host[:planes]
     t0 = time.perf_counter()
-    oracle.apply(slab, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
-                 steps=wl.steps, ndim=wl.ndim)
+    ref = oracle.apply(slab, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                       steps=wl.steps, ndim=wl.ndim)
     dt = time.perf_counter() - t0
     pts = slab.size * wl.steps
-    return {"value": round(pts / dt / 1e9, 6), "unit": "Gpoints/s", "cores": 1,
-            "kind": "oracle", "seconds": round(dt, 2),
-            "sample": "%dx%dx%d z-slab of the headline input, %d steps, fp64 single thread"
-                      % (slab.shape + (wl.steps,))}
+    out = {"value": round(pts / dt / 1e9, 6), "unit": "Gpoints/s", "cores": 1,
+           "kind": "oracle", "seconds": round(dt, 2),
+           "sample": "%dx%dx%d z-slab of the headline input, %d steps, fp64 single thread"
+                     % (slab.shape + (wl.steps,))}
+    valid = planes - wl.radius * wl.steps
+    if y_gpu is not None and wl.boundary == 0 and valid > 0:
+        err = float(np.abs(ref[:valid] - y_gpu[:valid].astype(np.float64)).max())
+        base = 1e-5 if wl.dtype == "f32" else 1e-12
+        tol = base * max(wl.steps, 1) * max(1.0, float(np.abs(slab).max()))
+        out["check"] = {"planes": valid, "points": int(ref[:valid].size),
+                        "max_abs_err": err, "tolerance": tol, "pass": bool(err <= tol)}
+    return out
 
 
 def main() -> int:
@@ -368,7 +401,9 @@ def main() -> int:
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, head.x_host, head.w, args.cpu_planes)
+        planes = min(args.cpu_planes, wl.dims[0])
+        y_gpu = head.y[:planes].cpu().numpy() if wl.ndim == 3 and wl.batch == 1 else None
+        cpu = cpu_baseline(wl, head.x_host, head.w, planes, y_gpu)
         log("[bench] cpu oracle: %s" % cpu)
     head.close()
     torch.cuda.empty_cache()
@@ -423,6 +458,7 @@ def main() -> int:
         "effective_gbs": fig["effective_gbs"],
         "roofline": roofline,
         "tuned": tuned,
+        "host": host_info(torch),
         "cpu_baseline": cpu,
         "copy_probe": probe,
         "workloads": others,

@@ -292,3 +292,63 @@ def test_maximum_size_star_1024_cubed(depth):
     ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius,
                               boundary=wl.boundary, steps=wl.steps)
     report("max size depth %d (%d samples)" % (depth, len(pts)), got, ref, tolerance(wl, x))
+
+
+GUARD_CASES = [
+    # name, dims, steps: star fused + trailing single step, 2D box fused, 2D star, box3
+    ("c3", (18, 40, 136), 3),
+    ("paper", (70, 260), 3),
+    ("c1", (40, 68), 2),
+    ("c5", (10, 12, 128), 2),
+]
+
+
+@pytest.mark.parametrize("name,dims,steps", GUARD_CASES, ids=[c[0] for c in GUARD_CASES])
+def test_guard_band_and_input_every_family(name, dims, steps):
+    """Multi-launch calls (ping-pong through the plan's grid, fused passes) write only
+    inside `out` (NaN canaries on both sides stay NaN) and never write `in`."""
+    n = 1 if name == "c5" else None
+    wl, (x, w, k) = _case(name, dims, n, steps)
+    dev = torch.device("cuda:0")
+    xt = torch.from_numpy(x).to(dev)
+    pad = 8192
+    buf = torch.full((x.size + 2 * pad,), float("nan"), dtype=xt.dtype, device=dev)
+    y = buf[pad:pad + x.size].view(x.shape)
+    lead = x.shape[: x.ndim - wl.ndim]
+    batch = int(np.prod(lead)) if len(lead) else 1
+    desc = B.make_desc(wl.ndim, wl.dims, batch=batch, channels=wl.channels,
+                       dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
+                       radius=wl.radius, boundary=wl.boundary)
+    plan = B.Plan(desc)
+    try:
+        print("[case] guard %s %s steps=%d kernel=%s depth=%d" % (
+            name, dims, steps, plan.info().kernel.decode(), plan.info().temporal_depth),
+            flush=True)
+        plan.run(xt, y, w, steps=steps)
+        torch.cuda.synchronize()
+    finally:
+        plan.close()
+    assert torch.isnan(buf[:pad]).all() and torch.isnan(buf[pad + x.size:]).all()
+    assert np.array_equal(xt.cpu().numpy(), x)
+    report("guard %s" % name, y.cpu().numpy().astype(np.float64), oracle_full(wl, x, w),
+           tolerance(wl, x))
+
+
+RAGGED = [
+    # streaming families on the extents 17, 63, 65, 257 (x a multiple of 16 bytes)
+    ("c3", (17, 63, 260), 3),
+    ("c3", (65, 17, 68), 2),
+    ("c2", (63, 65, 20), 3),
+    ("c4", (17, 65, 256), None),
+    ("paper", (257, 260), 3),
+    ("paper", (63, 1028), 2),
+]
+
+
+@pytest.mark.parametrize("name,dims,steps", RAGGED,
+                         ids=["%s-%s" % (r[0], "x".join(map(str, r[1]))) for r in RAGGED])
+def test_ragged_extents(name, dims, steps):
+    wl, (x, w, k) = _case(name, dims, None, steps)
+    got, info = run_library(wl, x, w, k)
+    print("[info] %s" % info, flush=True)
+    report("ragged %s %s" % (name, dims), got, oracle_full(wl, x, w, k), tolerance(wl, x, k))
