@@ -21,8 +21,9 @@ accepted: rocprofv3 can fault in its own teardown after the program has finished
 
 ``--write`` turns the raw outputs in OUT into the summaries under ``profiles/``: one
 text file per kernel and workload, giving the commands, the kernel statistics and the
-derived traffic, and ``counters.json``, which ``bench.py`` reads for the ``traffic``
-figure of its roofline object.  Each record carries the hash of the kernel's sources, so
+derived traffic, and ``counters.json`` (records of the summarised workloads are
+replaced, others kept), which ``bench.py`` reads for the ``traffic`` figure of its
+roofline object.  Each record carries the hash of the kernel's sources, so
 a record taken from older sources is ignored.
 """
 from __future__ import annotations
@@ -216,8 +217,16 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
                         % (sq["SQ_INSTS_VALU"][0] / sq["SQ_WAVES"][0],
                            sq.get("SQ_INSTS_LDS", (0,))[0] / sq["SQ_WAVES"][0]))
         print(fname, records["%s/%s" % (kern, w)])
-    with open(os.path.join(dest, "counters.json"), "w") as f:
-        json.dump(records, f, indent=1)
+    # Records of workloads not summarised in this call stay as they are (each carries its
+    # own source hash, so a stale one is ignored by its reader).
+    path = os.path.join(dest, "counters.json")
+    merged = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            merged = json.load(f)
+    merged.update(records)
+    with open(path, "w") as f:
+        json.dump(merged, f, indent=1)
     return records
 
 
