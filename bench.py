@@ -213,13 +213,13 @@ def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
     return {"bytes": nbytes, "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}
 
 
-def tune_context(torch, B, head, K: int, W: int) -> dict:
-    """stencil_tune on the headline workload (a fresh plan of the same description, the
-    same buffers), then K calls of the tuned plan timed like the headline.  Context only:
-    the headline value is the planner's default plan."""
+def tune_context(torch, B, head, K: int, W: int, reps: int = 10) -> dict:
+    """stencil_tune on a runner's workload (a fresh plan of the same description, the same
+    buffers; `reps` timed calls per candidate), then K calls of the tuned plan timed like
+    the default plan.  Context only: every reported value is the planner's default plan."""
     plan = B.Plan(head.plan.desc)
     try:
-        rep = plan.tune(head.x, head.y, head.w, steps=head.wl.steps, field=head.k, reps=10,
+        rep = plan.tune(head.x, head.y, head.w, steps=head.wl.steps, field=head.k, reps=reps,
                         stream=head.stream)
         info = plan.info()
         for _ in range(W):
@@ -433,6 +433,13 @@ def main() -> int:
                        launches_per_call=r.launches)
             if probe:
                 rec["frac_of_copy_probe"] = round(rec["effective_gbs"] / probe["gbs"], 4)
+            if not args.no_tune:
+                # the fastest valid launch configuration for this workload (the tuner's
+                # search), timed like the default plan above
+                tr = tune_context(torch, B, r, reps, 1 if name == "paper" else 3,
+                                  reps=3 if name == "paper" else 5)
+                rec["tuned"] = {k: tr[k] for k in ("chosen", "kernel", "candidates", "valid",
+                                                   "ms_per_call", "gpoints_per_s")}
             if name == "paper":
                 rec["ms_per_stencil_step"] = round(t / w2.steps, 5)
                 rec["context_a100_ms_per_step"] = PAPER_A100_MS_PER_STEP

@@ -115,7 +115,8 @@ typedef struct {
     int32_t valid;           /* 1: max_abs_err <= the tolerance (NaN is never valid) */
     int32_t reserved;
     double max_abs_err;      /* max over all points of |candidate - reference| */
-    double ms;               /* mean time of one call of `steps` steps; -1 if not timed */
+    double ms;               /* mean time of one call of `steps` steps in the fastest of
+                                the timing rounds; -1 if not timed (invalid) */
 } stencil_tune_entry;
 
 #define STENCIL_TUNE_MAX_CANDIDATES 16
@@ -174,10 +175,13 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
  *   Candidates (at most STENCIL_TUNE_MAX_CANDIDATES): the generic kernel itself; then,
  *     when the streaming variant can run the description and `in`, `out` and
  *     `coeff_field` are 16-byte aligned, every supported temporal depth (1, 2) x every
- *     tile of the one-step kernels (1, 2, or the single tile) x grid_scale in {-1, 0, 1}.
+ *     tile of the one-step kernels (1, 2, or the single tile) x grid_scale in
+ *     {-1, 0, 1, 2} (at most 13 candidates).
  *   Validity: a candidate's `out` must satisfy max_p |out - reference| <= tolerance (on the
  *     GPU, all points).  Invalid candidates are not timed.
- *   Timing: one untimed call, then `reps` calls between HIP events on `stream`; mean.
+ *   Timing: three rounds over the valid candidates (the validity run is each one's
+ *     warm-up); in each round, `reps` calls between HIP events on `stream`.  A
+ *     candidate's time is the mean call time of its fastest round.
  *   Result: the fastest valid candidate is fixed in the plan (variant, depth, tile,
  *     grid_scale; stencil_plan_query reports it), and `out` holds its result, i.e. `out`
  *     receives u_steps exactly as stencil_apply() would.

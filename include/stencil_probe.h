@@ -19,11 +19,12 @@ extern "C" {
 
 /*
  * stencil_probe_copy -- copy `bytes` bytes from `src` to `dst` on `stream` with 16-byte
- * vector loads and stores, one grid-stride kernel launch.
+ * non-temporal vector loads and stores, one kernel launch of one vector per thread.
  *   src, dst : device pointers, 16-byte aligned, non-overlapping (caller-owned).
  *   bytes    : a multiple of 16, >= 0.
  * Asynchronous.  Returns 0 on success, 1 for invalid arguments (checked on the host
- * before any HIP call), 2 if the launch failed.
+ * before any HIP call; also when `bytes` needs more than 2^31 - 1 workgroups of 4 KB), 2
+ * if the launch failed.
  */
 int stencil_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream);
 

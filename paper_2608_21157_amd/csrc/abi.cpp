@@ -427,7 +427,7 @@ stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
         for (int depth = 1; depth <= stencil::stream_max_depth(g); ++depth) {
             const bool tiles = depth == 1 && stencil::stream_has_tiles(g);
             for (int tile = tiles ? 1 : 0; tile <= (tiles ? 2 : 0); ++tile)
-                for (int scale = -1; scale <= 1; ++scale)
+                for (int scale = -1; scale <= 2; ++scale)
                     if (nc < STENCIL_TUNE_MAX_CANDIDATES)
                         cands[nc++] = {STENCIL_VARIANT_STREAM, depth, tile, scale};
         }
@@ -505,46 +505,61 @@ stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
         tol = c * double(steps) * (in_max > 1.0 ? in_max : 1.0);  // NaN input: NaN, no pass
     }
 
-    // ---- every candidate: validity gate, then timing ---------------------------------
-    int best = -1, last = -1;
-    double best_ms = 0.0;
+    // ---- every candidate through the validity gate --------------------------------------
+    bool valid[STENCIL_TUNE_MAX_CANDIDATES] = {};
+    double errs[STENCIL_TUNE_MAX_CANDIDATES] = {};
+    double ms[STENCIL_TUNE_MAX_CANDIDATES];
+    int last = -1;
     for (int i = 0; i < nc; ++i) {
         if ((st = run(cands[i], out)) != STENCIL_OK)
             return abort_with(st);
         last = i;
-        double err = 0.0;
-        if ((st = max_abs(out, ref, &err)) != STENCIL_OK)
+        if ((st = max_abs(out, ref, &errs[i])) != STENCIL_OK)
             return abort_with(st);
-        const bool valid = err <= tol;  // false for NaN
-        double ms = -1.0;
-        if (valid) {
+        valid[i] = errs[i] <= tol;  // false for NaN
+        ms[i] = -1.0;
+    }
+
+    // ---- timing: kTuneRounds interleaved rounds over the valid candidates; a candidate's
+    // time is the mean of `reps` calls in its fastest round, so that a clock or cache
+    // transient during one candidate's turn does not decide the choice
+    constexpr int kTuneRounds = 3;
+    for (int round = 0; round < kTuneRounds; ++round) {
+        for (int i = 0; i < nc; ++i) {
+            if (!valid[i])
+                continue;
             if ((e = hipEventRecord(e0, stream)) != hipSuccess)
                 return abort_with(hip_fail(e, "hipEventRecord"));
             for (int r = 0; r < reps; ++r)
                 if ((st = run(cands[i], out)) != STENCIL_OK)
                     return abort_with(st);
+            last = i;
             float total = 0.f;
             if ((e = hipEventRecord(e1, stream)) != hipSuccess ||
                 (e = hipEventSynchronize(e1)) != hipSuccess ||
                 (e = hipEventElapsedTime(&total, e0, e1)) != hipSuccess)
                 return abort_with(hip_fail(e, "timing events"));
-            ms = double(total) / reps;
-            if (best < 0 || ms < best_ms) {
-                best = i;
-                best_ms = ms;
-            }
+            const double t = double(total) / reps;
+            if (ms[i] < 0 || t < ms[i])
+                ms[i] = t;
         }
-        if (report != nullptr) {
+    }
+    int best = -1;
+    for (int i = 0; i < nc; ++i)
+        if (valid[i] && (best < 0 || ms[i] < ms[best]))
+            best = i;
+    if (report != nullptr) {
+        for (int i = 0; i < nc; ++i) {
             stencil_tune_entry &r = report->entry[i];
             r.variant = cands[i].variant;
             r.temporal_depth = cands[i].depth;
             r.tile = cands[i].tile;
             r.grid_scale = cands[i].grid_scale;
-            r.valid = valid ? 1 : 0;
-            r.max_abs_err = err;
-            r.ms = ms;
-            report->count = i + 1;
+            r.valid = valid[i] ? 1 : 0;
+            r.max_abs_err = errs[i];
+            r.ms = ms[i];
         }
+        report->count = nc;
     }
     if (report != nullptr)
         report->tolerance = tol;

@@ -62,11 +62,11 @@ def tune(wl, x, w, k, *, tolerance_=-1.0, reps=2, offset=0):
 
 
 TUNE_CASES = [
-    # name, dims, steps, candidates: generic + depth 1 (tiles x 3 scales) + depth 2 (3 scales)
-    ("c3", (40, 48, 256), 3, 1 + 2 * 3 + 3),
-    ("c2", (24, 40, 64), 3, 1 + 2 * 3 + 3),
-    ("c4", (12, 20, 512), None, 1 + 2 * 3),
-    ("paper", (96, 512), 3, 1 + 3 + 3),
+    # name, dims, steps, candidates: generic + depth 1 (tiles x 4 scales) + depth 2 (4 scales)
+    ("c3", (40, 48, 256), 3, 1 + 2 * 4 + 4),
+    ("c2", (24, 40, 64), 3, 1 + 2 * 4 + 4),
+    ("c4", (12, 20, 512), None, 1 + 2 * 4),
+    ("paper", (96, 512), 3, 1 + 4 + 4),
 ]
 
 
