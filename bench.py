@@ -170,8 +170,12 @@ def figures(wl, ms_per_call: float) -> dict:
     bytes_pt = wl.itemsize * (2 + (1 if wl.has_field else 0))
     gpts = pts / (ms_per_call * 1e-3) / 1e9
     gbs = pts * bytes_pt / (ms_per_call * 1e-3) / 1e9
+    # run-compulsory: the fields read once and the output written once per call, however
+    # many steps the call takes (a secondary reading; the sweep figure above is graded)
+    run_gbs = wl.points_per_step * bytes_pt / (ms_per_call * 1e-3) / 1e9
     return {"ms_per_call": round(ms_per_call, 5), "gpoints_per_s": round(gpts, 2),
-            "effective_gbs": round(gbs, 1), "frac_of_8tbs": round(gbs / HBM_PEAK_GBS, 4)}
+            "effective_gbs": round(gbs, 1), "frac_of_8tbs": round(gbs / HBM_PEAK_GBS, 4),
+            "run_compulsory_gbs": round(run_gbs, 1)}
 
 
 def spin_up(torch, stream, seconds=0.3) -> float:
@@ -428,6 +432,7 @@ def main() -> int:
             fl = r.flushed(2 if name == "paper" else 10, flush)
             rec = figures(w2, t)
             rec["flushed_median_ms"] = round(statistics.median(fl), 5)
+            rec["flushed_min_ms"] = round(min(fl), 5)
             rec["flushed_gpoints_per_s"] = figures(w2, statistics.median(fl))["gpoints_per_s"]
             rec.update(kernel=r.kernel, variant=r.variant, depth=r.depth,
                        launches_per_call=r.launches)
@@ -463,6 +468,7 @@ def main() -> int:
                    "kernel": head.kernel, "variant": head.variant,
                    "temporal_depth": head.depth, "parallelism": "single GPU"},
         "effective_gbs": fig["effective_gbs"],
+        "run_compulsory_gbs": fig["run_compulsory_gbs"],
         "roofline": roofline,
         "tuned": tuned,
         "host": host_info(torch),
