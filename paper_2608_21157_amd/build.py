@@ -1,12 +1,14 @@
 """Build the HIP library ``libstencil.so`` for gfx950 with hipcc.
 
 Every source under ``csrc/`` is compiled to an object in ``_build/`` (in parallel) and
-linked into ``libstencil.so`` next to this file.  ``build()`` always recompiles.
+linked into ``libstencil.so`` next to this file.  ``build()`` always recompiles.  A
+kernel that uses scratch memory fails the build.
 """
 from __future__ import annotations
 
 import concurrent.futures
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -36,13 +38,35 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the HIP library cannot be built")
 
 
+def scratch_kernels(remarks: str) -> list:
+    """Kernels that the compiler's resource-usage remarks report with scratch memory
+    (private arrays or spills moved out of registers)."""
+    out, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            out.append((name, int(m.group(1))))
+    return out
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc()] + lang + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    remarks = ["-Rpass-analysis=kernel-resource-usage"] if src.endswith(".hip") else []
+    cmd = [hipcc()] + lang + FLAGS + remarks + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr))
+    # Every kernel here keeps its queues and accumulators in registers; a kernel that the
+    # compiler moved to scratch memory runs an order of magnitude slower, so it is a
+    # build error rather than a silent slowdown.
+    bad = scratch_kernels(r.stderr)
+    if bad:
+        raise RuntimeError("%s: kernels using scratch memory: %s" % (
+            src, ", ".join("%s (%d B/lane)" % b for b in bad)))
     return obj
 
 
