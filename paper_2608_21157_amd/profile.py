@@ -54,6 +54,15 @@ SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_VALU",
                "SQ_ACTIVE_INST_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT",
                "SQ_LDS_IDX_ACTIVE")
 PAPER_STEPS = 64  # stencil steps per call of the paper workload under the profiler
+# SQ_WAVE_CYCLES counts wave residency in units of 4 cycles and SQ_BUSY_CYCLES sums the
+# busy cycles of the shader engines (8 CUs each on MI355X), so the mean resident waves
+# per CU is 4 * WAVE_CYCLES / BUSY_CYCLES / 8.  Check: the fused star kernel on c3 keeps
+# exactly 11 waves per CU for its whole run, and this gives 10.9.
+CUS_PER_SE = 8
+
+
+def occupancy(wave_cycles: float, busy_cycles: float) -> float:
+    return 4.0 * wave_cycles / busy_cycles / CUS_PER_SE
 
 
 def bench_args(workload: str, timed: bool) -> list:
@@ -212,6 +221,11 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
             if sq.get("SQ_LDS_IDX_ACTIVE", (0,))[0] > 0:
                 f.write("  LDS cycles stalled on bank conflicts: %.1f %% of LDS-active cycles\n"
                         % (100 * sq["SQ_LDS_BANK_CONFLICT"][0] / sq["SQ_LDS_IDX_ACTIVE"][0]))
+            if sq.get("SQ_BUSY_CYCLES", (0,))[0] > 0 and "SQ_WAVE_CYCLES" in sq:
+                f.write("  mean resident waves per CU: %.1f  (4 x SQ_WAVE_CYCLES / SQ_BUSY_CYCLES"
+                        " / %d CUs per shader engine)\n"
+                        % (occupancy(sq["SQ_WAVE_CYCLES"][0], sq["SQ_BUSY_CYCLES"][0]),
+                           CUS_PER_SE))
             if sq.get("SQ_INSTS_VALU", (0,))[0] > 0 and sq.get("SQ_WAVES", (0,))[0] > 0:
                 f.write("  VALU instructions per wave: %.0f; LDS instructions per wave: %.0f\n"
                         % (sq["SQ_INSTS_VALU"][0] / sq["SQ_WAVES"][0],
