@@ -250,6 +250,29 @@ def tune_context(torch, B, head, K: int, W: int, reps: int = 10) -> dict:
     return out
 
 
+def slab_context(torch, B, inputs, stream, gpus=8, reps=20) -> dict:
+    """One GPU's share of the headline under a z-slab decomposition over `gpus` GPUs: its
+    512/gpus owned planes plus the 2R planes on each side that one fused two-step pass
+    reads from its neighbours, timed for one pass (context for the multi-GPU design; the
+    halo exchange itself is not run)."""
+    wl = inputs.WORKLOADS["c3"]
+    own = wl.dims[0] // gpus
+    halo = 2 * wl.radius  # planes per side for two fused steps
+    slab = wl.resized((own + 2 * halo,) + tuple(wl.dims[1:]), steps=2)
+    r = Runner(torch, B, inputs, slab, stream)
+    spin_up(torch, stream, 0.1)
+    t = r.timed(reps, 3) / reps
+    kernel = r.kernel
+    r.close()
+    torch.cuda.empty_cache()
+    owned = own * wl.dims[1] * wl.dims[2] * slab.steps
+    plane_mib = wl.dims[1] * wl.dims[2] * wl.itemsize / 2 ** 20
+    return {"dims": list(slab.dims), "owned_planes": own, "halo_planes_per_side": halo,
+            "ms_per_pass": round(t, 5), "kernel": kernel,
+            "owned_gpoints_per_s": round(owned / (t * 1e-3) / 1e9, 2),
+            "halo_mib_per_face": round(halo * plane_mib, 1)}
+
+
 def miopen_context(torch, wl, x_host, w, reps=5):
     """Time torch's convolution (MIOpen on ROCm) on the same workload, one stencil step per
     call: the MI355X counterpart of the paper's cuDNN dense reference.  Context only; its
@@ -454,6 +477,8 @@ def main() -> int:
             log("[bench] %s: %s" % (name, rec))
             r.close()
             torch.cuda.empty_cache()
+        others["c3_slab_of_8"] = slab_context(torch, B, inputs, stream)
+        log("[bench] c3_slab_of_8: %s" % others["c3_slab_of_8"])
         del flush
 
     line = {
