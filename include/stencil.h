@@ -102,7 +102,9 @@ typedef struct {
     int32_t temporal_depth;  /* steps fused per launch */
     int64_t scratch_bytes;   /* device bytes the plan allocates for steps > 1 */
     const char *kernel;      /* base name of the dominant GPU kernel (static string) */
-    int32_t tile;            /* tile in use: 0 (the kernel has one), 1 or 2 */
+    int32_t tile;            /* the description's tile; where the plan's kernel is a
+                                one-step kernel with two tiles and the description says 0,
+                                the tile the planner resolved it to (1 or 2) */
     int32_t grid_scale;      /* workgroup-count exponent in use */
 } stencil_plan_info;
 

@@ -261,7 +261,10 @@ stencil_status stencil_plan_query(stencil_plan_t plan, stencil_plan_info *info)
     info->temporal_depth = p->depth;
     info->scratch_bytes = int64_t(p->scratch_bytes);
     info->kernel = p->kernel;
-    info->tile = p->geo.tile;
+    // the plan's tile; 0 resolved to the default where the plan runs a one-step kernel
+    // with two tiles
+    const int resolved = p->variant == STENCIL_VARIANT_STREAM ? stencil::stream_tile(p->geo, p->depth) : 0;
+    info->tile = resolved != 0 ? resolved : p->geo.tile;
     info->grid_scale = p->geo.grid_scale;
     return STENCIL_OK;
 }

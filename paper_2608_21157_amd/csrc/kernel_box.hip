@@ -341,9 +341,9 @@ bool box_stream_supported(const Geometry &g)
 hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, const void *field,
                              const void *w, hipStream_t stream)
 {
-    // 4 rows per lane by default (with the chunking above, 4 rows measured at least as
-    // fast as 8 on c4, c5 and c5b); the plan's tile forces 4 (tile 1) or 8 (tile 2)
-    const int ty = g.tile == 2 ? 8 : 4;
+    // 4 rows per lane (tile 1, the default: with the chunking above, 4 rows measured at
+    // least as fast as 8 on c4, c5 and c5b) or 8 (tile 2)
+    const int ty = stream_tile(g, 1) == 2 ? 8 : 4;
     if (g.dtype == STENCIL_F32)
         return ty == 4 ? launch_ty<float, 4>(g, src, dst, field, w, stream)
                        : launch_ty<float, 8>(g, src, dst, field, w, stream);

@@ -365,7 +365,7 @@ template <typename T, int R, int TY, bool ZAXIS, int CP>
 hipError_t launch_cp(const Geometry &g, const void *src, void *dst, const void *w,
                      hipStream_t stream)
 {
-    const bool large = g.tile == 2 || (g.tile == 0 && ZAXIS);
+    const bool large = stream_tile(g, 1) == 2;
     if (large)
         return launch_shape<T, R, TY, ZAXIS, CP, 16, 8, 1>(g, src, dst, w, stream);
     return launch_shape<T, R, TY, ZAXIS, CP, 16, 4, 1>(g, src, dst, w, stream);

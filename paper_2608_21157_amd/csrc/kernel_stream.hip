@@ -33,6 +33,19 @@ bool stream_has_tiles(const Geometry &g)
     return box_stream_supported(g) || star_stream_supported(g);
 }
 
+int stream_tile(const Geometry &g, int depth)
+{
+    if (depth != 1 || !stream_has_tiles(g))
+        return 0;
+    if (g.tile != 0)
+        return g.tile;
+    // defaults, measured on MI355X: the 3D box runs 4 rows per lane (tile 1); the star runs
+    // 64 x 64 tiles in 3D (tile 2) and 64 x 32 tiles in 2D (tile 1)
+    if (box_stream_supported(g))
+        return 1;
+    return g.ndim == 3 ? 2 : 1;
+}
+
 const char *stream_kernel_name(const Geometry &g, int depth)
 {
     if (box_stream_supported(g))

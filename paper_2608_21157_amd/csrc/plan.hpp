@@ -107,6 +107,11 @@ hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const 
 // Whether the one-step streaming kernel of this geometry offers two tiles (tile 1 / 2).
 bool stream_has_tiles(const Geometry &g);
 
+// The tile a streaming launch of `depth` steps runs: for a one-step kernel with two tiles,
+// the plan's tile or, for 0, the family default (1 or 2); 0 for kernels with one tile.
+// The launchers and stencil_plan_query both use it.
+int stream_tile(const Geometry &g, int depth);
+
 // max |a - b| over n elements of the given dtype (max |a| when b is NULL), computed on the
 // GPU.  `partial` is device memory for kCheckPartials doubles; the result lands in
 // partial[0] (NaN if any difference is NaN).
