@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 PAPER_STEPS_TIMED = 256
+ALU_PEAK_TFLOPS = 78.6
 # The paper's per-step latencies for its 2D radius-3 fp64 box on 10240^2, on an NVIDIA
 # A100-PCIE-40GB (Sec. "RQ3: Case Study on Stencil Computation"): context, not a target.
 PAPER_A100_MS_PER_STEP = {"best_generated_kernel": 4.71, "cudnn_implicit_precomp_gemm": 7.23}
@@ -250,6 +251,21 @@ def tune_context(torch, B, head, K: int, W: int, reps: int = 10) -> dict:
     return out
 
 
+def alu_roofline(wl, launches_per_call: int, avg_launch_ms: float) -> dict:
+    """The flop side of a call's launches: algorithmic flops (2 per offset and point-step,
+    plus 1 for the coefficient field) per launch over the average launch time.  Peak:
+    256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz = 78.6 TFLOP/s for fp32 or fp64 FMAs
+    issued one per lane; the build keeps packed fp32 out, which the published 157.3
+    TFLOP/s fp32 figure assumes."""
+    flops_pt = 2 * wl.npoints + (1 if wl.has_field else 0)
+    flops_per_launch = wl.points_per_step * (wl.steps / launches_per_call) * flops_pt
+    tflops = flops_per_launch / (avg_launch_ms * 1e-3) / 1e12
+    return {"bound": "alu", "achieved": round(tflops, 2), "peak": ALU_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(tflops / ALU_PEAK_TFLOPS, 4),
+            "published_fp32_peak": 157.3,
+            "algorithmic_flops_per_launch": int(flops_per_launch)}
+
+
 def slab_context(torch, B, inputs, stream, gpus=8, reps=20) -> dict:
     """One GPU's share of the headline under a z-slab decomposition over `gpus` GPUs: its
     512/gpus owned planes plus the 2R planes on each side that one fused two-step pass
@@ -418,6 +434,7 @@ def main() -> int:
                 "traffic": traffic, "kernel": head.kernel,
                 "avg_launch_ms": round(avg_launch_ms, 5),
                 "algorithmic_bytes_per_launch": int(algo_per_launch)}
+    roofline_alu = alu_roofline(wl, head.launches, avg_launch_ms)
     log("[bench] %s: %.4f ms/call, %.1f Gpoints/s, %.1f GB/s (%.1f%% of 8 TB/s)" % (
         wl.name, ms, fig["gpoints_per_s"], achieved, 100 * achieved / HBM_PEAK_GBS))
 
@@ -495,6 +512,7 @@ def main() -> int:
         "effective_gbs": fig["effective_gbs"],
         "run_compulsory_gbs": fig["run_compulsory_gbs"],
         "roofline": roofline,
+        "roofline_alu": roofline_alu,
         "tuned": tuned,
         "host": host_info(torch),
         "cpu_baseline": cpu,

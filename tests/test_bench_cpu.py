@@ -52,3 +52,19 @@ def test_counter_traffic_only_for_the_profiled_sources():
         else:
             assert got is None
     assert bench.counter_traffic("no_such_kernel", "c3", 1.0) is None
+
+
+def test_alu_roofline_of_the_fused_headline():
+    wl = WORKLOADS["c3"]                      # 25-point star, two launches of two steps
+    r = bench.alu_roofline(wl, 2, 0.336)
+    flops = 512 ** 3 * 2 * 50                 # points x fused steps x 2 flops per offset
+    assert r["algorithmic_flops_per_launch"] == flops
+    assert r["achieved"] == pytest.approx(flops / 0.336e-3 / 1e12, abs=0.01)
+    assert r["peak"] == pytest.approx(256 * 4 * 16 * 2 * 2.4e9 / 1e12, abs=0.05)
+    assert r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-3)
+
+
+def test_alu_roofline_counts_the_field_multiply():
+    wl = WORKLOADS["c4"]                      # 27-point box with k[p], one step
+    r = bench.alu_roofline(wl, 1, 1.0)
+    assert r["algorithmic_flops_per_launch"] == 512 ** 3 * (2 * 27 + 1)
