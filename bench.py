@@ -8,10 +8,17 @@ call, inputs already resident in HBM.  The metric is stencil points per second
 kernel against the compulsory-traffic roofline (each point read once and written once
 per stencil step: 8 bytes per point-step in fp32).
 
-Prints one JSON line on stdout; progress goes to stderr.  Besides the headline it reports
-every other workload (2D 5-point, 3D 7-point x10, 27-point box with a coefficient field
-(periodic), depthwise 3x3x3 conv form in fp32 and fp64), a copy-probe ceiling, and the
-CPU oracle timed on a bounded slab of the headline input.
+Prints one JSON line on stdout; progress goes to stderr.  Besides the headline (with an
+HBM roofline object and its flop-side counterpart) it reports, as context:
+  * the CPU oracle timed on a bounded slab of the headline input, and checked against
+    the GPU result there;
+  * every other workload (2D 5-point, 3D 7-point x10, 27-point box with a coefficient
+    field (periodic), depthwise 3x3x3 conv form in fp32 and fp64, and the paper's own 2D
+    radius-3 fp64 box), back to back and with the caches flushed;
+  * stencil_tune's choice and timing for each workload;
+  * a copy-probe ceiling, MIOpen's convolution on the conv-form cases, and one GPU's slab
+    of an 8-way z decomposition of the headline.
+Every reported value is the planner's default plan.
 """
 from __future__ import annotations
 

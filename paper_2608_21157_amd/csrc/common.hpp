@@ -6,32 +6,13 @@
 
 namespace stencil {
 
-// 16 bytes of T: four floats or two doubles, loaded and stored as one dwordx4 access.
+// 16 bytes of T: four floats or two doubles, loaded and stored as one dwordx4 access
+// (through the buffer-resource helpers below).
 template <typename T>
 struct alignas(16) Vec16 {
     static constexpr int N = 16 / sizeof(T);
     T e[N];
 };
-
-template <typename T>
-__device__ __forceinline__ Vec16<T> load16(const T *p)
-{
-    return *reinterpret_cast<const Vec16<T> *>(p);
-}
-
-template <typename T>
-__device__ __forceinline__ void store16(T *p, const Vec16<T> &v)
-{
-    *reinterpret_cast<Vec16<T> *>(p) = v;
-}
-
-template <typename T>
-__device__ __forceinline__ void store16_nt(T *p, const Vec16<T> &v)
-{
-#pragma unroll
-    for (int i = 0; i < Vec16<T>::N; ++i)
-        __builtin_nontemporal_store(v.e[i], p + i);
-}
 
 // DPP controls of the GFX9 family that move data across the whole 64-lane wavefront.
 constexpr int kDppWaveShl1 = 0x130;  // lane i reads lane i + 1; lane 63 keeps `old`
