@@ -260,13 +260,11 @@ stencil_box2_tb2_kernel(
     const int x = xs + lane * VEC;
     const bool xin = x >= 0 && x < p.nx;
     const bool out_lane = xin && lane >= HXV && lane < 64 - HXV;
+    const int out_off = out_lane ? x * E : kOutOfRange;
     const int y0 = ch * p.yc;
     const int n = max(0, min(p.yc, p.ny - y0));
     const T *src = in + b * p.vol;
     T *dst = out + b * p.vol;
-    const unsigned img_bytes = unsigned(p.vol * E);
-    const auto rin = make_rsrc(src, img_bytes);
-    const auto rout = make_rsrc(dst, img_bytes);
     const T *wb = w + (b % p.channels) * (NW * NW);
 
     const bool first = lane == 0, last = lane == 63;
@@ -287,16 +285,25 @@ stencil_box2_tb2_kernel(
         hx[k] = wrap_x(first ? xs - (k + 1) * VEC : xs + 64 * VEC + k * VEC, hok[k]);
         hok[k] = hok[k] && (first || last);
     }
-    auto row_off = [&](int y, int &own, int (&ho)[HXV]) {
-        bool ok = y >= 0 && y < p.ny;
+    // Addressing: a buffer resource per row, built from wave-uniform values only (scalar
+    // work), and per-lane byte offsets within a row that never change.  A row outside
+    // the grid (zero boundary) or past the chunk's input gets zero records, so its loads
+    // return zero; an invalid lane offset is past any row.  Against per-lane offsets into
+    // one image-wide resource: 145 -> 117 VGPRs and 3% less time per step (10240^2 fp64,
+    // radius 3).
+    const int own_off = own_ok ? xo * E : kOutOfRange;
+    int halo_off[HXV];
+#pragma unroll
+    for (int k = 0; k < HXV; ++k)
+        halo_off[k] = hok[k] ? hx[k] * E : kOutOfRange;
+    const unsigned row_bytes = unsigned(p.nx * E);
+    auto row_rsrc = [&](int y, bool live) {
+        bool ok = live && y >= 0 && y < p.ny;
         if (PERIODIC) {
             y = wrap_index(y, p.ny);
-            ok = true;
+            ok = live;
         }
-        own = (ok && own_ok) ? (y * p.nx + xo) * E : kOutOfRange;
-#pragma unroll
-        for (int k = 0; k < HXV; ++k)
-            ho[k] = (ok && hok[k]) ? (y * p.nx + hx[k]) * E : kOutOfRange;
+        return make_rsrc(src + (long long)(ok ? y : 0) * p.nx, ok ? row_bytes : 0u);
     };
 
     // input rows y0 - 2R .. y0 + yc - 1 + 2R; u1 rows y0 - R .. y0 + yc - 1 + R
@@ -305,13 +312,12 @@ stencil_box2_tb2_kernel(
     Vec16<T> qv[PF], hcur[HXV], hnxt[HXV];
 #pragma unroll
     for (int s = 0; s < PF; ++s) {
-        int own, ho[HXV];
-        row_off(y0 - 2 * R + s, own, ho);
-        qv[s] = bload16<T>(rin, own);
+        const auto rr = row_rsrc(y0 - 2 * R + s, true);
+        qv[s] = bload16<T>(rr, own_off);
         if (s == 0) {
 #pragma unroll
             for (int k = 0; k < HXV; ++k)
-                hnxt[k] = bload16<T>(rin, ho[k]);
+                hnxt[k] = bload16<T>(rr, halo_off[k]);
         }
     }
     T acc1[NS][VEC], acc2[NS][VEC];
@@ -402,19 +408,14 @@ stencil_box2_tb2_kernel(
         for (int i = 0; i < HXV; ++i)
             hcur[i] = hnxt[i];
         {
-            int o1, h1[HXV];
-            row_off(y0 - 2 * R + k + 1, o1, h1);
+            const auto rr = row_rsrc(y0 - 2 * R + k + 1, k + 1 < nin);
 #pragma unroll
             for (int i = 0; i < HXV; ++i)
-                hnxt[i] = bload16<T>(rin, k + 1 < nin ? h1[i] : kOutOfRange);
+                hnxt[i] = bload16<T>(rr, halo_off[i]);
         }
         T ext[NX];
         extend(own, hcur, ext, std::false_type{});
-        {
-            int o2, h2[HXV];
-            row_off(y0 - 2 * R + k + PF, o2, h2);
-            qv[j] = bload16<T>(rin, k + PF < nin ? o2 : kOutOfRange);
-        }
+        qv[j] = bload16<T>(row_rsrc(y0 - 2 * R + k + PF, k + PF < nin), own_off);
 #pragma unroll
         for (int a = 0; a < NW; ++a) {
             const int r1 = k - a;
@@ -444,8 +445,10 @@ stencil_box2_tb2_kernel(
                 v.e[e] = acc2[s2][e];
                 acc2[s2][e] = T(0);
             }
-            bstore16<T, STORE_CP>(rout, (out_lane && r2 >= 0 && r2 < n)
-                                            ? ((y0 + r2) * p.nx + x) * E : kOutOfRange, v);
+            const bool live = r2 >= 0 && r2 < n;
+            bstore16<T, STORE_CP>(
+                make_rsrc(dst + (long long)(live ? y0 + r2 : 0) * p.nx, live ? row_bytes : 0u),
+                out_off, v);
         }
     };
 
