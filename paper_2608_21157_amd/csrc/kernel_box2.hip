@@ -230,9 +230,9 @@ __global__ __launch_bounds__(256) void stencil_box2_stream_kernel(
 // boundary u1 is zero outside the grid, exactly as if it had been written and re-read.
 // Input row k feeds u1 row k - a (both relative to the chunk), which feeds u2 row
 // (k - 2R) - a; with the input queue, both accumulator sets rotate with period 2R + 1.
-// Three wavefronts per SIMD stated explicitly: the compiler then allocates 145 instead of
-// 149 registers for fp64 radius 3 and the kernel ran 2.3% faster; asking for four spills
-// 17 registers and ran 9% slower.
+// At least three wavefronts per SIMD stated explicitly: with per-row buffer resources the
+// kernel needs 117 registers for fp64 radius 3 (121 without the hint), which gives four.
+// A four-wave hint makes radius 4 spill to scratch.
 template <typename T, int R, bool PERIODIC, int STORE_CP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void
 stencil_box2_tb2_kernel(
@@ -475,9 +475,9 @@ int lanes_per_row(const Geometry &g, int vec)
     return (nxv >= 2 && 64 % nxv == 0) ? int(nxv) : 0;
 }
 
-// Wavefront count of a launch: at most one round of the waves the GPU holds at once
-// (`resident`, scaled by the plan's grid_scale), in whole chunks per image.  A second,
-// partly filled round left the GPU idle for most of its length: on 10240^2 fp64, radius 3,
+// Wavefront count of a launch: at most `target` waves (whole rounds of the waves the GPU
+// holds at once, scaled by the plan's grid_scale), in whole chunks per image.  A partly
+// filled last round leaves the GPU idle for most of its length: on 10240^2 fp64, radius 3,
 // 4128 waves against 3072 resident ran 1.34 rounds.
 inline long long whole_chunks(long long target, long long per_image, long long max_chunks)
 {
@@ -532,7 +532,11 @@ Box2Params make_tb2_params(const Geometry &g, int resident_waves)
     p.rg = 1;
     p.batch = g.batch;
     p.channels = g.channels;
-    const long long target = scaled_target(resident_waves, g.grid_scale);
+    // two rounds of whole chunks: on 10240^2 fp64, radius 3, 0.2747 ms per step for one
+    // round, 0.2695 for two, 0.2691 for three, 0.272 for six or eight (the later rounds
+    // even out the chunk tails; below 32R rows the 4R-row start-up of each chunk costs
+    // more than that)
+    const long long target = scaled_target(2LL * resident_waves, g.grid_scale);
     const long long per_image = g.batch * p.segs;
     const long long nchunks =  // >= 32R rows per chunk
         whole_chunks(target, per_image, (p.ny + 32 * R - 1) / (32 * R));
