@@ -261,6 +261,23 @@ def test_paper_workload_full_size_sampled():
     assert np.isfinite(got).all()
 
 
+def test_2d_image_beyond_the_streaming_limit_runs_generic():
+    """A 2D fp64 image over 1 GiB (11600 x 11600) exceeds the 32-bit byte offsets of the
+    2D box kernels: the planner falls back to the generic kernel, which indexes in 64 bits.
+    Two steps (ping-pong through the plan's scratch), sampled against the oracle."""
+    wl = WORKLOADS["paper"].resized((11600, 11600), steps=2)
+    assert wl.points_per_step * wl.itemsize > (1 << 30)
+    x, w, _ = inputs.make(wl)
+    got, info = run_library(wl, x, w)
+    print("[info] %s" % info, flush=True)
+    assert info["kernel"] == "stencil_generic_kernel"
+    pts = sample_points(wl, x, 200, seed=5)
+    ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                              steps=wl.steps, ndim=2)
+    report("2D beyond the streaming limit (%d samples)" % len(pts), gather(got, pts, wl), ref,
+           tolerance(wl, x))
+
+
 @pytest.mark.parametrize("depth", [2, 1], ids=["fused", "one-step"])
 def test_maximum_size_star_1024_cubed(depth):
     """The largest grid the tests drive: 1024^3 fp32 (2^30 points, 4 GiB per grid, eight
