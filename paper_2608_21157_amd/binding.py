@@ -117,10 +117,14 @@ def stencil_apply(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int 
                   radius: int, boundary: int, steps: int, stream: int | None) -> None:
     """``inp``/``out``/``coeff_field``: device addresses; ``coeffs``: a host buffer (numpy
     array or ctypes pointer) of the plan's dtype; ``stream``: a hipStream_t handle."""
-    d = (ctypes.c_int64 * 3)(*(list(dims) + [0] * (3 - len(dims))))
+    d = dims if isinstance(dims, ctypes.Array) else _dims3(dims)
     cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
     _check(load().stencil_apply(plan, inp, out, d, cp, coeff_field, radius, boundary, steps,
                                 stream))
+
+
+def _dims3(dims) -> ctypes.Array:
+    return (ctypes.c_int64 * 3)(*(list(dims) + [0] * (3 - len(dims))))
 
 
 def stencil_tune(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int | None,
@@ -180,6 +184,8 @@ class Plan:
         self.desc = desc
         self.handle = stencil_plan(desc)
         self.dims = tuple(desc.dims[i] for i in range(desc.ndim))
+        self._dims_c = _dims3(self.dims)  # built once: run() is on the latency path
+        self._coeffs = (None, None)       # last weight array and its host address
         self._stream = None
 
     def info(self) -> StencilPlanInfo:
@@ -191,7 +197,11 @@ class Plan:
             stream = torch.cuda.current_stream()
         sh = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
         self._stream = stream
-        stencil_apply(self.handle, x.data_ptr(), y.data_ptr(), self.dims, coeffs,
+        # the same array object keeps its buffer; the library compares the weights' bytes
+        # on every call, so values changed in place are still uploaded
+        if self._coeffs[0] is not coeffs:
+            self._coeffs = (coeffs, coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs)
+        stencil_apply(self.handle, x.data_ptr(), y.data_ptr(), self._dims_c, self._coeffs[1],
                       None if field is None else field.data_ptr(), self.desc.radius,
                       self.desc.boundary, steps, sh)
 
@@ -218,6 +228,7 @@ class Plan:
 
     def close(self) -> None:
         """Wait for the last stream this plan ran on, then free the plan."""
+        self._coeffs = (None, None)
         if self.handle:
             if self._stream is not None and hasattr(self._stream, "synchronize"):
                 self._stream.synchronize()

@@ -140,7 +140,8 @@ def test_misaligned_pointers_fall_back():
 
 
 def test_plan_reuse_with_changing_weights():
-    """One plan, two weight sets in a row on one stream: each call sees its own weights."""
+    """One plan, two weight sets in a row on one stream (distinct arrays, then one array
+    changed in place): each call sees its own weights."""
     wl, (x, w, k) = _case("c4", (8, 9, 256), None, None)
     dev = torch.device("cuda:0")
     xt = torch.from_numpy(x).to(dev)
@@ -154,6 +155,13 @@ def test_plan_reuse_with_changing_weights():
         for ww in (w, w2, w):
             y = torch.empty_like(xt)
             plan.run(xt, y, ww, steps=1, field=kt)
+            outs.append((ww, y))
+        # one array object whose values change in place between calls
+        wm = w.copy()
+        for ww in (w, w2):
+            wm[...] = ww
+            y = torch.empty_like(xt)
+            plan.run(xt, y, wm, steps=1, field=kt)  # copies the weights before returning
             outs.append((ww, y))
         torch.cuda.synchronize()
         for ww, y in outs:
