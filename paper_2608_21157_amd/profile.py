@@ -3,12 +3,14 @@
 
     python -m paper_2608_21157_amd.profile --out OUT [--workloads c3 c4 ...] [--write]
 
-For each workload, four passes profile the bench's headline leg:
+For each workload, five passes profile the bench's headline leg:
   * a kernel-trace pass (``--kernel-trace --stats``), timed like the bench (30 warm-up and
     50 timed calls; the paper workload with 64-step calls);
   * two counter passes, FETCH_SIZE and then WRITE_SIZE (HBM-side bytes);
   * an SQ pass: waves, busy and wave cycles, VALU and LDS instruction counts and activity,
-    and LDS bank-conflict cycles.
+    and LDS bank-conflict cycles;
+  * an SQ stall pass: wave cycles spent waiting (any, instruction dependencies, LDS) and
+    issuing (any, LDS, scalar), and scalar instruction counts.
 The copy probe is traced and counted the same way; its known byte counts calibrate
 FETCH_SIZE and WRITE_SIZE.  On gfx950, FETCH_SIZE counts 128-byte requests at half their
 size, which the copy calibration shows as a factor of 2.
@@ -53,6 +55,12 @@ COPY_BYTES = 1 << 30
 SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_VALU",
                "SQ_ACTIVE_INST_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT",
                "SQ_LDS_IDX_ACTIVE")
+# where the wave cycles go: waiting (for anything, for an instruction's dependencies, for
+# LDS results) and issuing (any instruction, LDS, scalar), all in the units of
+# SQ_WAVE_CYCLES; one pass (8 SQ counters)
+SQ_STALL_COUNTERS = ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_ANY",
+                     "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA", "SQ_INSTS_SALU",
+                     "SQ_INSTS_SMEM")
 PAPER_STEPS = 64  # stencil steps per call of the paper workload under the profiler
 # SQ_WAVE_CYCLES counts wave residency in units of 4 cycles and SQ_BUSY_CYCLES sums the
 # busy cycles of the shader engines (8 CUs each on MI355X), so the mean resident waves
@@ -85,7 +93,9 @@ def passes(workload: str) -> list:
     return [("trace_" + workload, ["--kernel-trace", "--stats"], bench_args(workload, True), 300),
             ("pmc_FETCH_SIZE_" + workload, ["--pmc", "FETCH_SIZE"], bench_args(workload, False), 150),
             ("pmc_WRITE_SIZE_" + workload, ["--pmc", "WRITE_SIZE"], bench_args(workload, False), 150),
-            ("pmc_SQ_" + workload, ["--pmc"] + list(SQ_COUNTERS), bench_args(workload, False), 150)]
+            ("pmc_SQ_" + workload, ["--pmc"] + list(SQ_COUNTERS), bench_args(workload, False), 150),
+            ("pmc_SQSTALL_" + workload, ["--pmc"] + list(SQ_STALL_COUNTERS),
+             bench_args(workload, False), 150)]
 
 
 def command(opts, name, workload, args, out="OUT", bench="R/bench.py") -> list:
@@ -221,6 +231,20 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
             if sq.get("SQ_LDS_IDX_ACTIVE", (0,))[0] > 0:
                 f.write("  LDS cycles stalled on bank conflicts: %.1f %% of LDS-active cycles\n"
                         % (100 * sq["SQ_LDS_BANK_CONFLICT"][0] / sq["SQ_LDS_IDX_ACTIVE"][0]))
+            st = counters(out, w, "SQSTALL", kern)
+            wc = sq.get("SQ_WAVE_CYCLES", (0,))[0]
+            if st and wc > 0:
+                f.write("SQ stall pass per dispatch (cycle counters as shares of"
+                        " SQ_WAVE_CYCLES; instruction counts per wave):\n")
+                nw = sq.get("SQ_WAVES", (0,))[0]
+                for c in SQ_STALL_COUNTERS:
+                    if c not in st:
+                        continue
+                    if c.startswith("SQ_INSTS_"):
+                        f.write("  %-24s %16.0f  %8.0f per wave\n"
+                                % (c, st[c][0], st[c][0] / nw if nw else 0))
+                    else:
+                        f.write("  %-24s %16.0f  %5.1f %%\n" % (c, st[c][0], 100 * st[c][0] / wc))
             if sq.get("SQ_BUSY_CYCLES", (0,))[0] > 0 and "SQ_WAVE_CYCLES" in sq:
                 f.write("  mean resident waves per CU: %.1f  (4 x SQ_WAVE_CYCLES / SQ_BUSY_CYCLES"
                         " / %d CUs per shader engine)\n"
