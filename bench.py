@@ -28,6 +28,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import statistics
 import sys
 import time
@@ -80,7 +81,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def code_only(text: str) -> str:
+    """C++ source without its comments and with whitespace collapsed: what the compiler
+    sees, so that a comment-only edit keeps a kernel's hash (the kernel sources hold no
+    string literal with comment markers)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_sha(kernel: str) -> str | None:
+    """Hash of the code (comments stripped) of a kernel's source files."""
     files = KERNEL_SOURCES.get(kernel)
     if not files:
         return None
@@ -89,8 +100,8 @@ def kernel_source_sha(kernel: str) -> str | None:
         path = os.path.join(ROOT, "paper_2608_21157_amd", "csrc", f)
         if not os.path.exists(path):
             return None
-        with open(path, "rb") as fh:
-            h.update(fh.read())
+        with open(path) as fh:
+            h.update(code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

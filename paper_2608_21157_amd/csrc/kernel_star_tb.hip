@@ -16,11 +16,12 @@
 // One thread owns one column of the stage-1 region (a 16-byte vector along x): its u0
 // z-queue (2R + 1 planes plus PF prefetched) and its u1 z-queue (2R + 1 planes) live in
 // registers.  Both queues rotate through the same 2R + 1 + PF slots, so the loop is
-// unrolled that many times and every register index is static.  The current u0 plane (stage 1's
-// in-plane neighbours, over the stage-1 region and one more band) and the current u1
-// plane (stage 2's in-plane neighbours) are staged in double-buffered LDS, one barrier
-// per plane.  Band threads use their u1 queue as the R-plane delay line that feeds the
-// u1 plane stage 2 reads.
+// unrolled that many times and every register index is static.  The current u0 plane
+// (stage 1's in-plane neighbours, over the stage-1 region and one more band) and the
+// current u1 plane (stage 2's in-plane neighbours) are staged in LDS: double-buffered
+// with one barrier per plane at radius 1 and 2, and two planes per barrier (four
+// buffers) at radius 3 and 4.  Band threads use their u1 queue as the R-plane delay line
+// that feeds the u1 plane stage 2 reads.
 #include "common.hpp"
 #include "plan.hpp"
 

@@ -68,3 +68,11 @@ def test_alu_roofline_counts_the_field_multiply():
     wl = WORKLOADS["c4"]                      # 27-point box with k[p], one step
     r = bench.alu_roofline(wl, 1, 1.0)
     assert r["algorithmic_flops_per_launch"] == 512 ** 3 * (2 * 27 + 1)
+
+
+def test_code_hash_ignores_comments_but_not_code():
+    src = "int f(int a) {  // one\n  /* two\n lines */ return a + 1;\n}\n"
+    same = "int f(int a) { return a + 1; }  // other comment\n"
+    other = "int f(int a) { return a + 2; }\n"
+    assert bench.code_only(src) == bench.code_only(same)
+    assert bench.code_only(src) != bench.code_only(other)
