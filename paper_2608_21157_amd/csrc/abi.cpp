@@ -225,8 +225,9 @@ stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan)
         variant = stream_ok ? STENCIL_VARIANT_STREAM : STENCIL_VARIANT_GENERIC;
     if (variant == STENCIL_VARIANT_STREAM && !stream_ok)
         return fail(STENCIL_ERR_UNSUPPORTED,
-                    "the streaming kernels need a 3D grid with a supported shape and radius "
-                    "and an x extent they can tile");
+                    "no streaming kernel runs this description (they cover the 3D 3x3x3 box, "
+                    "2D boxes and 2D/3D stars up to radius 4, a coefficient field only with "
+                    "the 3D box, and need an x extent they can tile in 16-byte vectors)");
     const int max_depth = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_max_depth(g) : 1;
     const int dflt = (variant == STENCIL_VARIANT_STREAM) ? stencil::stream_default_depth(g) : 1;
     int depth = desc->temporal_depth == 0 ? dflt : desc->temporal_depth;
@@ -263,7 +264,8 @@ stencil_status stencil_plan_query(stencil_plan_t plan, stencil_plan_info *info)
     info->kernel = p->kernel;
     // the plan's tile; 0 resolved to the default where the plan runs a one-step kernel
     // with two tiles
-    const int resolved = p->variant == STENCIL_VARIANT_STREAM ? stencil::stream_tile(p->geo, p->depth) : 0;
+    const int resolved =
+        p->variant == STENCIL_VARIANT_STREAM ? stencil::stream_tile(p->geo, p->depth) : 0;
     info->tile = resolved != 0 ? resolved : p->geo.tile;
     info->grid_scale = p->geo.grid_scale;
     return STENCIL_OK;
