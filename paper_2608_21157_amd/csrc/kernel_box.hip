@@ -8,7 +8,8 @@
 // Mapping (no LDS, no barriers):
 //   * a wavefront owns a row segment of 64 lanes x 16 bytes (256 floats / 128 doubles)
 //     along x -- or, for narrower rows, 64/lpr whole rows side by side -- times TY rows
-//     per lane along y, and streams a chunk of z planes;
+//     per lane along y, and streams a chunk of z planes (even chunks upwards, odd chunks
+//     downwards, so neighbouring chunks read their shared halo plane at about the same time);
 //   * every input plane is read once per wavefront as TY + 2 coalesced 16-byte row loads
 //     per lane (the two extra rows are the y halo, shared through L2 with the wave that
 //     owns them);
@@ -64,13 +65,16 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
 
+    // logical tile order: x segment fastest, then row block, then z chunk, then volume,
+    // so that the segments of one row block (which read each other's x halo) and the
+    // neighbouring row blocks run on the same XCD at about the same time
     int t = xcd_logical_block(blockIdx.x, p.nblocks);
+    const int seg = t % p.segs;
+    t /= p.segs;
     const int yg = t % p.ygroups;
     t /= p.ygroups;
     const int zi = t % p.nzc;
-    t /= p.nzc;
-    const int seg = t % p.segs;
-    const long long b = t / p.segs;
+    const long long b = t / p.nzc;
     const int yw = yg * 4 + wave;
     if (yw >= p.ywaves)
         return;  // whole wavefront leaves; the kernel has no barriers
@@ -87,10 +91,16 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     T *dst = out + b * p.vol;
     const T *kf = FIELD ? field + b * p.vol : nullptr;
     const T *wb = w + (b % p.channels) * 27;
+    // Odd chunks stream downwards, so that two neighbouring chunks reach the plane they
+    // share as a halo at about the same time (the second read then hits L2).  Streaming
+    // down mirrors the z offsets: weight plane a is then applied as plane 2 - a.
+    const bool up = (zi & 1) == 0;
+    auto zin = [&](int k) { return up ? z0 - 1 + k : z0 + n - k; };   // input plane k
+    auto zout = [&](int q) { return up ? z0 + q : z0 + n - 1 - q; };  // output plane q
     T W[27];
 #pragma unroll
     for (int j = 0; j < 27; ++j)
-        W[j] = wb[j];
+        W[j] = wb[up ? j : (2 - j / 9) * 9 + j % 9];
 
     // byte offsets of input rows y0 - 1 .. y0 + TY within a plane; rows outside the grid
     // (zero boundary) get an offset past the resource and read as zero
@@ -138,7 +148,7 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     T halo[NR];
     Vec16<T> kv[TY];
     {
-        const auto r0 = plane_rsrc(z0 - 1);
+        const auto r0 = plane_rsrc(zin(0));
 #pragma unroll
         for (int i = 0; i < NR; ++i) {
             rows[i] = bload16<T>(r0, ro[i]);
@@ -147,17 +157,18 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     }
     auto load_field = [&](int q) {
         if (FIELD) {
-            const auto rk = make_rsrc(kf + (long long)(z0 + q) * plane, plane_bytes);
+            const auto rk = make_rsrc(kf + (long long)zout(q) * plane, plane_bytes);
 #pragma unroll
             for (int o = 0; o < TY; ++o)
                 kv[o] = bload16<T, kNonTemporal>(rk, ((y0 + o) * p.nx + x) * E);
         }
     };
 
-    // Fold input plane k (z_in = z0 - 1 + k) into the accumulators, reloading each row
-    // register with the next plane right after its last use.  Offset (a, bb, c) in weight
-    // order is (oz, oy, ox) = (a - 1, bb - 1, c - 1); the input point feeds output plane
-    // q = k - a (slot q mod 3) and output row o = i - bb.  Planes q < 0 are skipped
+    // Fold input plane k (z_in = zin(k)) into the accumulators, reloading each row
+    // register with the next plane right after its last use.  Offset (a, bb, c) in the
+    // (mirrored when streaming down) weight order is (oz, oy, ox) = (a - 1, bb - 1, c - 1);
+    // the input point feeds output plane q = k - a (slot q mod 3, z = zout(q)) and output
+    // row o = i - bb.  Planes q < 0 are skipped
     // (prologue only).
     // CHECK: skip output planes q < 0 (the prologue); in the steady state every q = k - a
     // is accumulated, since planes q >= n never complete and are never written (no branch
@@ -165,7 +176,7 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     // branch is kept (measured: c5 +1.2%, c5b +2.3% without it; c4, with the field, -1.3%).
     auto fold = [&](int k, auto slot_of_a, auto check) {
         const bool more = k + 1 <= n + 1;
-        const auto rn = plane_rsrc(z0 + k);
+        const auto rn = plane_rsrc(zin(k + 1));
 #pragma unroll
         for (int i = 0; i < NR; ++i) {
             T r[VEC + 2];
@@ -209,7 +220,7 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     // are dropped) and clear the slot; the field rows are read here rather than prefetched,
     // which keeps the kernel at three wavefronts per SIMD
     auto emit = [&](int q, int s) {
-        const auto rd = make_rsrc(dst + (long long)(z0 + q) * plane, plane_bytes);
+        const auto rd = make_rsrc(dst + (long long)zout(q) * plane, plane_bytes);
         load_field(q);
 #pragma unroll
         for (int o = 0; o < TY; ++o) {

@@ -377,3 +377,21 @@ def test_ragged_extents(name, dims, steps):
     got, info = run_library(wl, x, w, k)
     print("[info] %s" % info, flush=True)
     report("ragged %s %s" % (name, dims), got, oracle_full(wl, x, w, k), tolerance(wl, x, k))
+
+
+BOX3_CHUNKS = [("c4", 2), ("c4", 1), ("c5", 2), ("c5b", 1)]
+
+
+@pytest.mark.parametrize("name,gs", BOX3_CHUNKS, ids=["%s-s%d" % c for c in BOX3_CHUNKS])
+def test_box3_z_chunks_both_directions(name, gs):
+    """The 27-point box streams even z chunks upwards and odd ones downwards (mirrored z
+    weights).  37 planes in chunks of 4 (grid scale 2: ten chunks, the last one plane) or
+    of 8 (grid scale 1: five chunks, the last five planes); periodic with a field (c4) and
+    zero boundary with per-channel weights (c5, c5b); every point against the oracle."""
+    wl, (x, w, k) = _case(name, (37, 10, 256 if name == "c4" else 128),
+                          None if name == "c4" else 1, None)
+    print("[case] box3 chunks %s dims=%s grid_scale=%d" % (name, wl.dims, gs), flush=True)
+    got, info = run_library(wl, x, w, k, grid_scale=gs)
+    assert info["kernel"] == "stencil_box3_stream_kernel", info
+    report("box3 chunks %s s%d %s" % (name, gs, info), got, oracle_full(wl, x, w, k),
+           tolerance(wl, x, k))
