@@ -332,23 +332,31 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
                     p->device, dev);
     p->device = dev;
     const size_t wbytes = size_t(g.channels) * size_t(g.npts) * g.elt;
+    // each resource is created on its own, so that a call after a failed first use
+    // completes the set instead of running with part of it missing
     if (p->d_coeff == nullptr) {
         if ((e = hipMalloc(&p->d_coeff, wbytes)) != hipSuccess) {
             p->d_coeff = nullptr;
             return fail(STENCIL_ERR_NO_MEMORY, "hipMalloc(%zu) for weights: %s", wbytes,
                         hipGetErrorString(e));
         }
+        p->coeff_valid = false;
+    }
+    if (p->h_stage == nullptr) {
         if ((e = hipHostMalloc(&p->h_stage, wbytes, hipHostMallocDefault)) != hipSuccess) {
             p->h_stage = nullptr;
             return fail(STENCIL_ERR_NO_MEMORY, "hipHostMalloc(%zu): %s", wbytes,
                         hipGetErrorString(e));
         }
+    }
+    if (p->stage_done == nullptr) {
         if ((e = hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming)) != hipSuccess) {
             p->stage_done = nullptr;
             return hip_fail(e, "hipEventCreateWithFlags");
         }
-        p->h_cache.assign(wbytes, 0);
     }
+    if (p->h_cache.size() != wbytes)
+        p->h_cache.assign(wbytes, 0);
     if (launches > 1 && p->scratch == nullptr) {
         if ((e = hipMalloc(&p->scratch, p->scratch_bytes)) != hipSuccess) {
             p->scratch = nullptr;
