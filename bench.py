@@ -163,6 +163,36 @@ class Runner:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1)
 
+    def graph_timed(self, calls: int, reps: int) -> float:
+        """Milliseconds per call with `calls` back-to-back calls captured in one HIP graph
+        (torch.cuda.graph on the runner's stream) and the graph replayed `reps` times: what
+        a serving loop pays per call once the host-side launch cost is taken out.  The
+        plan has run before (its buffers exist, its weights are uploaded), so a captured
+        call holds kernel launches only."""
+        torch = self.torch
+        self.call()
+        self.stream.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=self.stream):
+            for _ in range(calls):
+                self.call_on(torch.cuda.current_stream())
+        self.plan._stream = self.stream
+        with torch.cuda.stream(self.stream):
+            g.replay()
+            self.stream.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            for _ in range(reps):
+                g.replay()
+            e1.record(self.stream)
+            e1.synchronize()
+        del g
+        return e0.elapsed_time(e1) / (reps * calls)
+
+    def call_on(self, stream):
+        self.plan.run(self.x, self.y, self.w, steps=self.wl.steps, field=self.k, stream=stream)
+
     def flushed(self, R: int, flush) -> list:
         """Per-call milliseconds with L2 and the Infinity Cache flushed before each call
         (the flush runs on the same stream, outside the events)."""
@@ -503,6 +533,12 @@ def main() -> int:
                                   reps=3 if name == "paper" else 5)
                 rec["tuned"] = {k: tr[k] for k in ("chosen", "kernel", "candidates", "valid",
                                                    "ms_per_call", "gpoints_per_s")}
+            if name in ("c1", "c2"):
+                # launch-bound workloads: the same calls replayed from a HIP graph
+                gms = r.graph_timed(50, 20)
+                rec["graph_replay"] = {"ms_per_call": round(gms, 5),
+                                       "gpoints_per_s": figures(w2, gms)["gpoints_per_s"],
+                                       "calls_per_graph": 50}
             if name == "paper":
                 rec["ms_per_stencil_step"] = round(t / w2.steps, 5)
                 rec["context_a100_ms_per_step"] = PAPER_A100_MS_PER_STEP
