@@ -395,3 +395,29 @@ def test_box3_z_chunks_both_directions(name, gs):
     assert info["kernel"] == "stencil_box3_stream_kernel", info
     report("box3 chunks %s s%d %s" % (name, gs, info), got, oracle_full(wl, x, w, k),
            tolerance(wl, x, k))
+
+
+RADIUS0 = [(B.STAR, 3, B.ZERO, False), (B.BOX, 3, B.PERIODIC, True),
+           (B.BOX, 2, B.ZERO, False), (B.STAR, 2, B.PERIODIC, False)]
+
+
+@pytest.mark.parametrize("shape,ndim,boundary,field", RADIUS0,
+                         ids=["%s%dd-%s%s" % ("star" if c[0] == B.STAR else "box", c[1],
+                                              "zero" if c[2] == B.ZERO else "per",
+                                              "-field" if c[3] else "") for c in RADIUS0])
+def test_radius_zero(shape, ndim, boundary, field):
+    """Radius 0, the degenerate stencil (the centre only): each step scales every point by
+    k w0.  Three steps over four volumes with two weight sets, every point against the
+    oracle (the planner runs the generic kernel here)."""
+    from dataclasses import replace
+    dims = (6, 10, 36) if ndim == 3 else (20, 36)
+    wl = replace(WORKLOADS["c4"].resized((6, 10, 36)), ndim=ndim, dims=dims, shape=shape,
+                 radius=0, boundary=boundary, steps=3, has_field=field, channels=2)
+    g = np.random.default_rng(41)
+    x = g.uniform(-1, 1, (4,) + dims).astype(np.float32)
+    w = g.uniform(-1, 1, (2, 1)).astype(np.float32)
+    k = g.uniform(0.5, 1.0, x.shape).astype(np.float32) if field else None
+    print("[case] radius 0 shape=%d ndim=%d boundary=%d field=%s" % (shape, ndim, boundary,
+                                                                    field), flush=True)
+    got, info = run_library(wl, x, w, k)
+    report("radius 0 %s" % info, got, oracle_full(wl, x, w, k), tolerance(wl, x, k))

@@ -429,3 +429,21 @@ def test_rejects_bad_arguments():
         oracle.apply(x, np.zeros(26), shape=BOX, radius=1)
     with pytest.raises(ValueError):
         oracle.apply_points(x, np.zeros(27), [[0, 3, 0, 0]], shape=BOX, radius=1)
+
+
+@pytest.mark.parametrize("shape", [STAR, BOX])
+@pytest.mark.parametrize("boundary", [ZERO, PERIODIC])
+def test_radius_zero_is_pointwise_scaling(shape, boundary):
+    """Radius 0 (the degenerate stencil: one offset, the centre) reduces every step to
+    u <- k * w0 * u, so s steps give (k w0)^s * u, with no neighbour and no boundary
+    effect; per channel for batched volumes."""
+    g = np.random.default_rng(31)
+    C = 3
+    x = g.uniform(-1, 1, (2 * C, 4, 5, 6))
+    w = g.uniform(-1, 1, (C, 1))
+    k = g.uniform(0.5, 1.0, x.shape)
+    got = oracle.apply(x, w, shape=shape, radius=0, boundary=boundary, steps=3, field=k,
+                       ndim=3, channels=C)
+    scale = np.repeat(w[:, 0], 1)[np.arange(2 * C) % C][:, None, None, None]
+    ref = (k * scale) ** 3 * x
+    assert np.allclose(got, ref, rtol=1e-14, atol=1e-15)
