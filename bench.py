@@ -378,8 +378,12 @@ def host_info(torch) -> dict:
     info = {"cpus": os.cpu_count(), "torch": torch.__version__}
     try:
         with open("/proc/cpuinfo") as f:
-            info["cpu"] = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
-    except (OSError, StopIteration):
+            lines = f.readlines()
+        info["cpu"] = next(l.split(":", 1)[1].strip() for l in lines if l.startswith("model name"))
+        mhz = [float(l.split(":", 1)[1]) for l in lines if l.startswith("cpu MHz")]
+        if mhz:
+            info["cpu_mhz"] = round(max(mhz))
+    except (OSError, StopIteration, ValueError):
         pass
     try:
         with open("/opt/rocm/.info/version") as f:
@@ -388,6 +392,7 @@ def host_info(torch) -> dict:
         pass
     try:
         info["gpu"] = torch.cuda.get_device_name(0)
+        info["gpu_arch"] = torch.cuda.get_device_properties(0).gcnArchName
     except Exception:
         pass
     return info
