@@ -199,7 +199,8 @@ class Runner:
         torch = self.torch
         out = []
         for i in range(R):
-            flush.fill_(float(i))
+            with torch.cuda.stream(self.stream):  # ordered before the events, not beside them
+                flush.fill_(float(i))
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(self.stream)
