@@ -251,6 +251,7 @@ def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
     lib.stencil_probe_copy.restype = ctypes.c_int
     a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").uniform_()
     b = torch.empty_like(a)
+    torch.cuda.synchronize()  # `a` is filled on torch's stream, the copies run on `stream`
     sh = stream.cuda_stream
     for _ in range(3):
         assert lib.stencil_probe_copy(a.data_ptr(), b.data_ptr(), nbytes, sh) == 0
