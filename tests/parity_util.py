@@ -33,6 +33,7 @@ def run_library(wl, x, w, k=None, *, steps=None, variant=B.VARIANT_AUTO, depth=0
     xt = torch.from_numpy(np.ascontiguousarray(x)).to(dev)
     yt = torch.full_like(xt, float("nan"))
     kt = None if k is None else torch.from_numpy(np.ascontiguousarray(k)).to(dev)
+    torch.cuda.synchronize()  # the NaN fill runs on torch's stream; the call may use another
     lead = xt.shape[: xt.dim() - wl.ndim]
     batch = int(np.prod(lead)) if len(lead) else 1
     desc = B.make_desc(wl.ndim, xt.shape[xt.dim() - wl.ndim:], batch=batch,
