@@ -243,29 +243,48 @@ def spin_up(torch, stream, seconds=0.3) -> float:
     return round(time.perf_counter() - t0, 3)
 
 
-def copy_probe(torch, stream, nbytes=1 << 30, reps=20):
+def copy_probe(torch, stream, nbytes=1 << 30, reps=20, kind="copy"):
+    """Achievable HBM throughput of a plain stream of the same shape as a stencil's: `copy`
+    (one array read, one written, `nbytes` each) or `triad` (two read, one written: the
+    mix of a stencil with a coefficient field).  GB/s counts every array once."""
     path = os.path.join(ROOT, "paper_2608_21157_amd", "libstencil_probe.so")
     lib = ctypes.CDLL(path)
-    lib.stencil_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
-                                       ctypes.c_void_p]
+    vp = ctypes.c_void_p
+    lib.stencil_probe_copy.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.stencil_probe_copy.restype = ctypes.c_int
+    lib.stencil_probe_triad.argtypes = [vp, vp, vp, ctypes.c_int64, vp]
+    lib.stencil_probe_triad.restype = ctypes.c_int
     a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").uniform_()
-    b = torch.empty_like(a)
-    torch.cuda.synchronize()  # `a` is filled on torch's stream, the copies run on `stream`
+    b = torch.empty_like(a).uniform_() if kind == "triad" else None
+    c = torch.empty_like(a)
+    torch.cuda.synchronize()  # the inputs are filled on torch's stream, the probe uses `stream`
     sh = stream.cuda_stream
+    if kind == "triad":
+        run = lambda: lib.stencil_probe_triad(a.data_ptr(), b.data_ptr(), c.data_ptr(), nbytes, sh)
+        arrays = 3
+    else:
+        run = lambda: lib.stencil_probe_copy(a.data_ptr(), c.data_ptr(), nbytes, sh)
+        arrays = 2
     for _ in range(3):
-        assert lib.stencil_probe_copy(a.data_ptr(), b.data_ptr(), nbytes, sh) == 0
+        assert run() == 0
     stream.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(reps):
-        lib.stencil_probe_copy(a.data_ptr(), b.data_ptr(), nbytes, sh)
+        run()
     e1.record(stream)
     e1.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    assert torch.equal(a, b)
-    del a, b
-    return {"bytes": nbytes, "ms": round(ms, 4), "gbs": round(2 * nbytes / ms / 1e6, 1)}
+    assert torch.equal(c, a * b if kind == "triad" else a)
+    del a, b, c
+    torch.cuda.empty_cache()
+    return {"kind": kind, "bytes": nbytes, "ms": round(ms, 4),
+            "gbs": round(arrays * nbytes / ms / 1e6, 1)}
+
+
+# The probe each one-step workload is read against: its own access mix at its own array
+# size (the multi-step workloads move fewer HBM bytes than their sweep figure counts).
+PATTERN_PROBES = {"c4": ("triad", 1 << 29), "c5": ("copy", 1 << 31), "c5b": ("copy", 1 << 30)}
 
 
 def tune_context(torch, B, head, K: int, W: int, reps: int = 10) -> dict:
@@ -513,6 +532,13 @@ def main() -> int:
         spin_up(torch, stream)  # the GPU idled during the CPU leg
         probe = copy_probe(torch, stream)
         log("[bench] copy probe: %s" % probe)
+        patterns = {}
+        for name, (kind, nbytes) in PATTERN_PROBES.items():
+            key = (kind, nbytes)
+            if key not in patterns:
+                patterns[key] = copy_probe(torch, stream, nbytes, kind=kind)
+                log("[bench] %s probe, %d MiB per array: %s" % (kind, nbytes >> 20,
+                                                                 patterns[key]))
         flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0")  # 1 GiB
         for name in ("c1", "c2", "c3", "c4", "c5", "c5b", "paper"):
             w2 = inputs.WORKLOADS[name]
@@ -534,6 +560,10 @@ def main() -> int:
                        launches_per_call=r.launches)
             if probe:
                 rec["frac_of_copy_probe"] = round(rec["effective_gbs"] / probe["gbs"], 4)
+            if name in PATTERN_PROBES:
+                pp = patterns[PATTERN_PROBES[name]]
+                rec["pattern_probe"] = pp
+                rec["frac_of_pattern_probe"] = round(rec["effective_gbs"] / pp["gbs"], 4)
             if not args.no_tune:
                 # the fastest valid launch configuration for this workload (the tuner's
                 # search), timed like the default plan above

@@ -1,5 +1,5 @@
 /*
- * stencil_probe.h -- HBM copy probe used to calibrate the stencil measurements.
+ * stencil_probe.h -- HBM probes used to calibrate the stencil measurements.
  *
  * The stencil kernels are judged against the compulsory-traffic roofline (each input
  * element read once, each output element written once).  This probe measures what a
@@ -27,6 +27,20 @@ extern "C" {
  * if the launch failed.
  */
 int stencil_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream);
+
+/*
+ * stencil_probe_triad -- dst[i] = a[i] * b[i] over `bytes` bytes of fp32 per array on
+ * `stream`: two streams read and one written, each element once, with the access shape
+ * of stencil_probe_copy.  It is the achievable ceiling for the two-read, one-write mix of
+ * a stencil with an output-indexed coefficient field (the input and the field read, the
+ * output written).
+ *   a, b, dst : device pointers, 16-byte aligned, `dst` overlapping neither (caller-owned).
+ *   bytes     : bytes of each array, a multiple of 16, >= 0.
+ * Asynchronous.  Returns 0 on success, 1 for invalid arguments (checked on the host
+ * before any HIP call), 2 if the launch failed.
+ */
+int stencil_probe_triad(const void *a, const void *b, void *dst, int64_t bytes,
+                        hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -1,5 +1,6 @@
 // probe_copy.hip -- 16-byte streaming copy: the achievable read+write HBM ceiling, and
-// the reference for scaling hardware byte counters.
+// the reference for scaling hardware byte counters; and a two-read, one-write stream of
+// the same shape, the ceiling for the access mix of a stencil with a coefficient field.
 //
 // Each thread copies one 16-byte vector with a non-temporal load and store; consecutive
 // workgroups cover consecutive 4 KB pieces.  Of the copies measured on MI355X this one is
@@ -23,7 +24,45 @@ __global__ __launch_bounds__(256) void stencil_probe_copy_kernel(const V4 *__res
         __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
+// Two streams read, one written (the mix of a stencil with a coefficient field):
+// dst = a * b elementwise in fp32, one 16-byte vector per thread, non-temporal.
+__global__ __launch_bounds__(256) void stencil_probe_triad_kernel(const V4 *__restrict__ a,
+                                                                  const V4 *__restrict__ b,
+                                                                  V4 *__restrict__ dst,
+                                                                  long long n)
+{
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i < n)
+        __builtin_nontemporal_store(__builtin_nontemporal_load(a + i) *
+                                        __builtin_nontemporal_load(b + i),
+                                    dst + i);
+}
+
+bool bad_args(const void *const *ptrs, int count, int64_t bytes)
+{
+    if (bytes < 0 || bytes % 16 != 0 || (bytes / 16 + 255) / 256 > 0x7fffffffLL)
+        return true;
+    for (int i = 0; i < count; ++i)
+        if (ptrs[i] == nullptr || (reinterpret_cast<uintptr_t>(ptrs[i]) & 15u))
+            return true;
+    return false;
+}
+
 }  // namespace
+
+extern "C" int stencil_probe_triad(const void *a, const void *b, void *dst, int64_t bytes,
+                                   hipStream_t stream)
+{
+    const void *ptrs[3] = {a, b, dst};
+    if (bad_args(ptrs, 3, bytes))
+        return 1;
+    const long long n = bytes / 16;
+    if (n == 0)
+        return 0;
+    stencil_probe_triad_kernel<<<dim3(unsigned((n + 255) / 256)), dim3(256), 0, stream>>>(
+        static_cast<const V4 *>(a), static_cast<const V4 *>(b), static_cast<V4 *>(dst), n);
+    return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int stencil_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream)
 {

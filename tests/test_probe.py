@@ -18,6 +18,9 @@ def probe():
     lib.stencil_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                        ctypes.c_void_p]
     lib.stencil_probe_copy.restype = ctypes.c_int
+    lib.stencil_probe_triad.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p]
+    lib.stencil_probe_triad.restype = ctypes.c_int
     return lib
 
 
@@ -30,6 +33,19 @@ def test_probe_rejects_invalid_arguments_before_any_hip_call():
     assert lib.stencil_probe_copy(A + 8, B_, 64, None) == 1      # misaligned source
     assert lib.stencil_probe_copy(A, B_ + 4, 64, None) == 1      # misaligned destination
     assert lib.stencil_probe_copy(A, B_, 0, None) == 0           # nothing to do, no launch
+
+
+def test_triad_rejects_invalid_arguments_before_any_hip_call():
+    lib = probe()
+    C = 0x7F0200000000
+    assert lib.stencil_probe_triad(None, B_, C, 64, None) == 1
+    assert lib.stencil_probe_triad(A, None, C, 64, None) == 1
+    assert lib.stencil_probe_triad(A, B_, None, 64, None) == 1
+    assert lib.stencil_probe_triad(A, B_, C, -16, None) == 1
+    assert lib.stencil_probe_triad(A, B_, C, 40, None) == 1       # not a multiple of 16
+    assert lib.stencil_probe_triad(A + 4, B_, C, 64, None) == 1   # misaligned input
+    assert lib.stencil_probe_triad(A, B_, C + 8, 64, None) == 1   # misaligned output
+    assert lib.stencil_probe_triad(A, B_, C, 0, None) == 0        # nothing to do, no launch
 
 
 @pytest.mark.gpu
@@ -46,3 +62,20 @@ def test_probe_copies_exactly(nbytes):
     stream.synchronize()
     assert torch.equal(dst[:nbytes], src[:nbytes])
     assert int(dst[nbytes:].abs().sum()) == 0   # nothing written past the end
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("nbytes", [16, 4096 + 16, (1 << 22) + 48])
+def test_triad_multiplies_exactly(nbytes):
+    import torch
+    lib = probe()
+    n = nbytes // 4
+    a = torch.rand(n + 16, device="cuda:0")
+    b = torch.rand(n + 16, device="cuda:0")
+    dst = torch.zeros(n + 16, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    assert lib.stencil_probe_triad(a.data_ptr(), b.data_ptr(), dst.data_ptr(), nbytes,
+                                   stream.cuda_stream) == 0
+    stream.synchronize()
+    assert torch.equal(dst[:n], a[:n] * b[:n])    # one fp32 product, correctly rounded
+    assert int((dst[n:] != 0).sum()) == 0         # nothing written past the end
