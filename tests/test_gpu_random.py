@@ -81,3 +81,26 @@ def test_random_description(seed):
     got, info = run_library(wl, x, w, k)
     print("[info] %s" % info, flush=True)
     report("random %d %s" % (seed, info), got, oracle_full(wl, x, w, k), tolerance(wl, x, k))
+
+
+@pytest.mark.parametrize("seed", SEEDS[:60])
+def test_random_description_forced_launch(seed):
+    """The same draws with a forced launch configuration: one step per launch, a drawn grid
+    scale (-2..2) and, for the one-step kernels that have two tiles, a drawn tile."""
+    wl, x, w, k = draw(seed)
+    g = np.random.default_rng(5000 + seed)
+    desc = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
+                       dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
+                       radius=wl.radius, boundary=wl.boundary, has_coeff_field=k is not None,
+                       temporal_depth=1)
+    plan = B.Plan(desc)
+    kernel = plan.info().kernel.decode()
+    plan.close()
+    tiles = kernel in ("stencil_star_stream_kernel", "stencil_box3_stream_kernel")
+    tile = int(g.integers(1, 3)) if tiles else 0
+    gs = int(g.integers(-2, 3))
+    print("[case] random %d forced: depth 1 tile %d grid_scale %d (%s)" % (seed, tile, gs,
+                                                                         kernel), flush=True)
+    got, info = run_library(wl, x, w, k, depth=1, tile=tile, grid_scale=gs)
+    report("random %d forced %s" % (seed, info), got, oracle_full(wl, x, w, k),
+           tolerance(wl, x, k))
