@@ -42,7 +42,7 @@ BENCH = os.path.join(ROOT, "bench.py")
 PROFILES = os.path.join(ROOT, "profiles")
 sys.path.insert(0, ROOT)
 
-WORKLOADS = ("c3", "c4", "c2", "c5", "c5b", "paper")
+WORKLOADS = ("c3", "c4", "c2", "c5", "c5b", "paper", "c1")
 KERNELS = {  # kernel base name -> short name of the summary file
     "stencil_star_stream_kernel": "star_stream",
     "stencil_star_tb2_kernel": "star_tb2",
