@@ -358,6 +358,23 @@ def slab_context(torch, B, inputs, stream, gpus=8, reps=20) -> dict:
             "halo_mib_per_face": round(halo * plane_mib, 1)}
 
 
+def deep_fusion_context(torch, B, inputs, stream, reps=20) -> dict:
+    """The c2 operator (fp32 7-point star, 10 steps) on 512^3, beyond the Infinity Cache:
+    the planner's four steps per pass against two (context for the temporal depth rule;
+    the c2 workload itself, 256^3, stays inside the cache and runs two)."""
+    wl = inputs.WORKLOADS["c2_512"]
+    out = {"dims": list(wl.dims), "steps": wl.steps}
+    for key, depth in (("planner", 0), ("two_per_pass", 2)):
+        r = Runner(torch, B, inputs, wl, stream, depth=depth)
+        spin_up(torch, stream, 0.1)
+        t = r.timed(reps, 10) / reps
+        out[key] = {"kernel": r.kernel, "depth": r.depth, "ms_per_call": round(t, 5),
+                    "gpoints_per_s": figures(wl, t)["gpoints_per_s"]}
+        r.close()
+        torch.cuda.empty_cache()
+    return out
+
+
 def miopen_context(torch, wl, x_host, w, reps=5):
     """Time torch's convolution (MIOpen on ROCm) on the same workload, one stencil step per
     call: the MI355X counterpart of the paper's cuDNN dense reference.  Context only; its
@@ -588,6 +605,8 @@ def main() -> int:
             torch.cuda.empty_cache()
         others["c3_slab_of_8"] = slab_context(torch, B, inputs, stream)
         log("[bench] c3_slab_of_8: %s" % others["c3_slab_of_8"])
+        others["c2_at_512_cubed"] = deep_fusion_context(torch, B, inputs, stream)
+        log("[bench] c2_at_512_cubed: %s" % others["c2_at_512_cubed"])
         del flush
 
     line = {

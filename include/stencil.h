@@ -83,7 +83,11 @@ typedef struct {
     int32_t has_coeff_field; /* 1: out[p] = k[p] * sum_j w[j] * u(p + O[j]); 0: no field */
     int32_t variant;         /* stencil_variant; 0 = AUTO */
     int32_t temporal_depth;  /* steps fused per launch where the variant supports it;
-                                0 = planner's choice, 1 = one launch per step */
+                                0 = planner's choice, 1 = one launch per step.  The
+                                streaming variant fuses up to 2 steps for 2D boxes and 3D
+                                stars, up to 4 for fp32 radius-1 3D stars; a larger value
+                                is STENCIL_ERR_UNSUPPORTED.  A call whose step count is not
+                                a multiple ends with a shallower pass */
     int32_t tile;            /* workgroup tile of the one-step streaming kernels that have
                                 two: 0 = planner's choice, 1 = the smaller, 2 = the larger
                                 (3D star: 32- or 64-row x-y tiles; 3D box: 4 or 8 rows per
@@ -121,7 +125,7 @@ typedef struct {
                                 the timing rounds; -1 if not timed (invalid) */
 } stencil_tune_entry;
 
-#define STENCIL_TUNE_MAX_CANDIDATES 16
+#define STENCIL_TUNE_MAX_CANDIDATES 20
 
 typedef struct {
     int32_t count;           /* candidates tried (entries filled) */
@@ -176,9 +180,10 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
  *     `in` for `steps` steps.
  *   Candidates (at most STENCIL_TUNE_MAX_CANDIDATES): the generic kernel itself; then,
  *     when the streaming variant can run the description and `in`, `out` and
- *     `coeff_field` are 16-byte aligned, every supported temporal depth (1, 2) x every
- *     tile of the one-step kernels (1, 2, or the single tile) x grid_scale in
- *     {-1, 0, 1, 2} (at most 13 candidates).
+ *     `coeff_field` are 16-byte aligned, every temporal depth among 1, 2 and 4 that the
+ *     description supports x every tile of the one-step kernels (1, 2, or the single
+ *     tile) x grid_scale in {-1, 0, 1, 2} (at most 17 candidates; a depth of 3 is
+ *     supported but not tried).
  *   Validity: a candidate's `out` must satisfy max_p |out - reference| <= tolerance (on the
  *     GPU, all points).  Invalid candidates are not timed.
  *   Timing: three rounds over the valid candidates (the validity run is each one's

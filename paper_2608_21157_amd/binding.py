@@ -26,7 +26,7 @@ VARIANT_NAMES = {VARIANT_GENERIC: "generic", VARIANT_STREAM: "stream"}
 
 EXPORTED = ("stencil_plan", "stencil_apply", "stencil_destroy", "stencil_plan_query",
             "stencil_num_points", "stencil_status_str", "stencil_last_error", "stencil_tune")
-TUNE_MAX_CANDIDATES = 16
+TUNE_MAX_CANDIDATES = 20
 
 
 class StencilDesc(ctypes.Structure):

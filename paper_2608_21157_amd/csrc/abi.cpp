@@ -437,7 +437,10 @@ stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
     const bool aligned = aligned16(in) && aligned16(out) &&
                          (coeff_field == nullptr || aligned16(coeff_field));
     if (aligned && stencil::stream_supported(g)) {
-        for (int depth = 1; depth <= stencil::stream_max_depth(g); ++depth) {
+        int depths[4];
+        const int nd = stencil::stream_tune_depths(g, depths);
+        for (int di = 0; di < nd; ++di) {
+            const int depth = depths[di];
             const bool tiles = depth == 1 && stencil::stream_has_tiles(g);
             for (int tile = tiles ? 1 : 0; tile <= (tiles ? 2 : 0); ++tile)
                 for (int scale = -1; scale <= 2; ++scale)

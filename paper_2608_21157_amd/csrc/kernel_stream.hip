@@ -11,7 +11,22 @@ bool stream_supported(const Geometry &g)
 
 int stream_max_depth(const Geometry &g)
 {
+    if (star_tbs_supported(g))
+        return 4;
     return (star_tb2_supported(g) || box2_tb2_supported(g)) ? 2 : 1;
+}
+
+int stream_tune_depths(const Geometry &g, int *depths)
+{
+    // three steps per pass is never the fastest where four are possible (measured on
+    // fp32 radius 1, 256^3 and 512^3), so the tuner skips it
+    int n = 0;
+    depths[n++] = 1;
+    if (stream_max_depth(g) >= 2)
+        depths[n++] = 2;
+    if (stream_max_depth(g) >= 4)
+        depths[n++] = 4;
+    return n;
 }
 
 int stream_default_depth(const Geometry &g)
@@ -22,6 +37,11 @@ int stream_default_depth(const Geometry &g)
     //   fp32 512^3:      R=1 643 -> 1205, R=2 617 -> 1005, R=3 598 -> 792, R=4 594 -> 699
     //   fp64 256x512^2:  R=1 332 -> 631,  R=2 301 -> 500,  R=3 307 -> 387, R=4 311 -> 338
     // 2D boxes: two steps per pass measured 1.26x faster per step (10240^2 fp64, radius 3)
+    // fp32 radius 1 with a working set beyond the Infinity Cache: four steps per pass
+    // (kernel_star_tbs.hip; 512^3, 10 steps: 1235 -> 1406-1471 Gpoints/s); inside it two
+    // (256^3, 10 steps: 1300 against 1230 with four)
+    if (star_tbs_supported(g) && streaming_stores(g))
+        return 4;
     if (box2_tb2_supported(g) || star_tb2_supported(g))
         return 2;
     return 1;
@@ -54,6 +74,8 @@ const char *stream_kernel_name(const Geometry &g, int depth)
         return "stencil_box2_tb2_kernel";
     if (box2_stream_supported(g))
         return "stencil_box2_stream_kernel";
+    if (star_tbs_supported(g) && depth >= 3)
+        return "stencil_star_tbs_kernel";
     if (star_tb2_supported(g) && depth == 2)
         return "stencil_star_tb2_kernel";
     if (star_stream_supported(g))
@@ -64,6 +86,8 @@ const char *stream_kernel_name(const Geometry &g, int depth)
 hipError_t launch_stream(const Geometry &g, const void *src, void *dst, const void *field,
                          const void *w, int depth, hipStream_t stream)
 {
+    if (depth >= 3 && star_tbs_supported(g))
+        return launch_star_tbs(g, src, dst, w, depth, stream);
     if (depth == 2 && star_tb2_supported(g))
         return launch_star_tb2(g, src, dst, w, stream);
     if (depth == 2 && box2_tb2_supported(g))

@@ -104,6 +104,15 @@ bool star_tb2_supported(const Geometry &g);
 hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,
                            hipStream_t stream);
 
+// Three or four star steps fused in one pass (3D, fp32, radius 1).
+bool star_tbs_supported(const Geometry &g);
+hipError_t launch_star_tbs(const Geometry &g, const void *src, void *dst, const void *w,
+                           int depth, hipStream_t stream);
+
+// Temporal depths stencil_tune tries for this geometry (ascending, at most 4 entries);
+// returns their number.
+int stream_tune_depths(const Geometry &g, int *depths);
+
 // Whether the one-step streaming kernel of this geometry offers two tiles (tile 1 / 2).
 bool stream_has_tiles(const Geometry &g);
 

@@ -27,6 +27,8 @@ field and batched channels):
   c5b the same recipe in fp64 at N=2 (separate draws).
   paper  the paper's own case: 2D box R=3 (49 points), 10240^2 fp64, ZERO (padding 3);
       weights not printed in the paper, so i.i.d. U[-1,1] normalised to sum|w| = 1.
+  c2_512  the c2 recipe on 512^3 (a working set beyond the Infinity Cache, where four
+      steps per pass pay off); context for the temporal-depth rule, not one of the five.
 """
 from __future__ import annotations
 
@@ -95,6 +97,8 @@ WORKLOADS = {
                     "conv", n=2),
     "paper": Workload("paper", 2, (10240, 10240), 1, 1, "f64", BOX, 3, ZERO, 10240, False, 7,
                       "box_uniform"),
+    "c2_512": Workload("c2_512", 3, (512, 512, 512), 1, 1, "f32", STAR, 1, ZERO, 10, False, 2,
+                       "star7"),
 }
 
 

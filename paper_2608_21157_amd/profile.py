@@ -42,10 +42,11 @@ BENCH = os.path.join(ROOT, "bench.py")
 PROFILES = os.path.join(ROOT, "profiles")
 sys.path.insert(0, ROOT)
 
-WORKLOADS = ("c3", "c4", "c2", "c5", "c5b", "paper", "c1")
+WORKLOADS = ("c3", "c4", "c2", "c5", "c5b", "paper", "c1", "c2_512")
 KERNELS = {  # kernel base name -> short name of the summary file
     "stencil_star_stream_kernel": "star_stream",
     "stencil_star_tb2_kernel": "star_tb2",
+    "stencil_star_tbs_kernel": "star_tbs",
     "stencil_box3_stream_kernel": "box3_stream",
     "stencil_box2_stream_kernel": "box2_stream",
     "stencil_box2_tb2_kernel": "box2_tb2",

@@ -421,3 +421,42 @@ def test_radius_zero(shape, ndim, boundary, field):
                                                                     field), flush=True)
     got, info = run_library(wl, x, w, k)
     report("radius 0 %s" % info, got, oracle_full(wl, x, w, k), tolerance(wl, x, k))
+
+
+TBS_CASES = [(d, n, bnd) for d, steps in ((4, (4, 5, 6, 7, 9)), (3, (3, 5)))
+             for n in steps for bnd in (B.ZERO, B.PERIODIC)]
+
+
+@pytest.mark.parametrize("depth,steps,bnd", TBS_CASES,
+                         ids=["d%d-s%d-%s" % (c[0], c[1], "zero" if c[2] == B.ZERO else "per")
+                              for c in TBS_CASES])
+def test_star_four_steps_per_pass(depth, steps, bnd):
+    """fp32 radius-1 3D stars with three or four steps fused per pass (trailing passes of
+    one or two steps for the remainder), ragged extents in every axis, every point."""
+    from dataclasses import replace
+    g = np.random.default_rng(200 + 10 * depth + steps)
+    for dims in ((23, 37, 72), (9, 3, 40)):
+        wl = replace(WORKLOADS["c2"].resized(dims, steps=steps), boundary=bnd)
+        x = g.uniform(-1, 1, dims).astype(np.float32)
+        w = g.uniform(-1, 1, (1, wl.npoints))
+        w = (w / np.abs(w).sum()).astype(np.float32)
+        print("[case] tbs depth=%d steps=%d bnd=%d dims=%s" % (depth, steps, bnd, dims),
+              flush=True)
+        got, info = run_library(wl, x, w, depth=depth)
+        assert info["kernel"] == "stencil_star_tbs_kernel" and info["depth"] == depth, info
+        report("tbs %s %s" % (dims, info), got, oracle_full(wl, x, w), tolerance(wl, x))
+
+
+def test_star_four_steps_per_pass_512_cubed():
+    """The planner's choice for an fp32 radius-1 star beyond the Infinity Cache: four
+    steps per pass.  512^3, 10 steps (4 + 4 + 2), sampled against the oracle."""
+    wl = WORKLOADS["c2_512"]
+    x, w, _ = inputs.make(wl)
+    print("[case] tbs 512^3 steps=%d" % wl.steps, flush=True)
+    got, info = run_library(wl, x, w)
+    assert info["kernel"] == "stencil_star_tbs_kernel" and info["depth"] == 4, info
+    pts = sample_points(wl, x, 300, seed=9)
+    ref = oracle.apply_points(x, w, pts, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                              steps=wl.steps, ndim=3)
+    report("tbs 512^3 (%d samples)" % len(pts), gather(got, pts, wl), ref, tolerance(wl, x))
+    assert np.isfinite(got).all()

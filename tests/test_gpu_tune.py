@@ -63,8 +63,9 @@ def tune(wl, x, w, k, *, tolerance_=-1.0, reps=2, offset=0):
 
 TUNE_CASES = [
     # name, dims, steps, candidates: generic + depth 1 (tiles x 4 scales) + depth 2 (4 scales)
+    # (+ depth 4, 4 scales, for fp32 radius-1 stars)
     ("c3", (40, 48, 256), 3, 1 + 2 * 4 + 4),
-    ("c2", (24, 40, 64), 3, 1 + 2 * 4 + 4),
+    ("c2", (24, 40, 64), 5, 1 + 2 * 4 + 4 + 4),
     ("c4", (12, 20, 512), None, 1 + 2 * 4),
     ("paper", (96, 512), 3, 1 + 4 + 4),
 ]

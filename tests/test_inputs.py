@@ -58,7 +58,7 @@ def test_paper_case_matches_golden():
     assert w.boundary == inputs.ZERO and w.shape == inputs.BOX
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c5b", "paper"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c5b", "paper", "c2_512"])
 def test_reduced_workloads_are_seeded_and_in_range(name):
     base = WORKLOADS[name]
     dims = (12, 10) if base.ndim == 2 else (6, 10, 12)
