@@ -50,6 +50,7 @@ KERNEL_SOURCES = {
     "stencil_box3_stream_kernel": ["kernel_box.hip", "common.hpp", "plan.hpp"],
     "stencil_star_stream_kernel": ["kernel_star.hip", "common.hpp", "plan.hpp"],
     "stencil_star_tb2_kernel": ["kernel_star_tb.hip", "common.hpp", "plan.hpp"],
+    "stencil_star_tbs_kernel": ["kernel_star_tbs.hip", "common.hpp", "plan.hpp"],
     "stencil_box2_stream_kernel": ["kernel_box2.hip", "common.hpp", "plan.hpp"],
     "stencil_box2_tb2_kernel": ["kernel_box2.hip", "common.hpp", "plan.hpp"],
     "stencil_generic_kernel": ["kernel_generic.hip", "plan.hpp"],

@@ -165,6 +165,25 @@ def fmt_cmds(workload: str) -> str:
     return "\n".join(lines) + "\n"
 
 
+def fused_depth(kernel: str, wl) -> int:
+    """Stencil steps per launch of the profiled kernel: 2 for the two-step kernels, the
+    planner's depth for the kernel of three or four steps (asked of the library, which
+    plans on the host), 1 for the one-step kernels."""
+    if "tb2" in kernel:
+        return 2
+    if "tbs" in kernel:
+        from paper_2608_21157_amd import binding as B
+        d = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
+                        dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
+                        radius=wl.radius, boundary=wl.boundary, has_coeff_field=wl.has_field)
+        h = B.stencil_plan(d)
+        try:
+            return int(B.stencil_plan_query(h).temporal_depth)
+        finally:
+            B.stencil_destroy(h)
+    return 1
+
+
 def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
     import bench
     from paper_2608_21157_amd.inputs import WORKLOADS as WL
@@ -194,7 +213,7 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
         fetch, nf = counters(out, w, "FETCH_SIZE", kern)["FETCH_SIZE"]
         write, nw = counters(out, w, "WRITE_SIZE", kern)["WRITE_SIZE"]
         sq = counters(out, w, "SQ", kern)
-        depth = 2 if "tb2" in kern else 1
+        depth = fused_depth(kern, wl)
         bytes_pt = wl.itemsize * (2 + (1 if wl.has_field else 0))
         algo = wl.points_per_step * depth * bytes_pt
         avg_ns = float(top["AverageNs"])
