@@ -85,8 +85,8 @@ typedef struct {
     int32_t temporal_depth;  /* steps fused per launch where the variant supports it;
                                 0 = planner's choice, 1 = one launch per step.  The
                                 streaming variant fuses up to 2 steps for 2D boxes and 3D
-                                stars, up to 4 for fp32 radius-1 3D stars; a larger value
-                                is STENCIL_ERR_UNSUPPORTED.  A call whose step count is not
+                                stars, up to 4 for fp32 and 3 for fp64 radius-1 3D stars;
+                                a larger value is STENCIL_ERR_UNSUPPORTED.  A call whose step count is not
                                 a multiple ends with a shallower pass */
     int32_t tile;            /* workgroup tile of the one-step streaming kernels that have
                                 two: 0 = planner's choice, 1 = the smaller, 2 = the larger
@@ -180,10 +180,10 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
  *     `in` for `steps` steps.
  *   Candidates (at most STENCIL_TUNE_MAX_CANDIDATES): the generic kernel itself; then,
  *     when the streaming variant can run the description and `in`, `out` and
- *     `coeff_field` are 16-byte aligned, every temporal depth among 1, 2 and 4 that the
- *     description supports x every tile of the one-step kernels (1, 2, or the single
- *     tile) x grid_scale in {-1, 0, 1, 2} (at most 17 candidates; a depth of 3 is
- *     supported but not tried).
+ *     `coeff_field` are 16-byte aligned, the temporal depths 1, 2 and the deepest the
+ *     description supports (3 or 4 for radius-1 3D stars; a depth of 3 is not tried
+ *     where 4 is possible) x every tile of the one-step kernels (1, 2, or the single
+ *     tile) x grid_scale in {-1, 0, 1, 2} (at most 17 candidates).
  *   Validity: a candidate's `out` must satisfy max_p |out - reference| <= tolerance (on the
  *     GPU, all points).  Invalid candidates are not timed.
  *   Timing: three rounds over the valid candidates (the validity run is each one's

@@ -12,20 +12,21 @@ bool stream_supported(const Geometry &g)
 int stream_max_depth(const Geometry &g)
 {
     if (star_tbs_supported(g))
-        return 4;
+        return star_tbs_max_depth(g);
     return (star_tb2_supported(g) || box2_tb2_supported(g)) ? 2 : 1;
 }
 
 int stream_tune_depths(const Geometry &g, int *depths)
 {
-    // three steps per pass is never the fastest where four are possible (measured on
-    // fp32 radius 1, 256^3 and 512^3), so the tuner skips it
+    // 1, 2 and the deepest: three steps per pass is never the fastest where four are
+    // possible (measured on fp32 radius 1, 256^3 and 512^3), so the tuner skips it there
     int n = 0;
     depths[n++] = 1;
-    if (stream_max_depth(g) >= 2)
+    const int dmax = stream_max_depth(g);
+    if (dmax >= 2)
         depths[n++] = 2;
-    if (stream_max_depth(g) >= 4)
-        depths[n++] = 4;
+    if (dmax >= 3)
+        depths[n++] = dmax;
     return n;
 }
 
@@ -37,11 +38,12 @@ int stream_default_depth(const Geometry &g)
     //   fp32 512^3:      R=1 643 -> 1205, R=2 617 -> 1005, R=3 598 -> 792, R=4 594 -> 699
     //   fp64 256x512^2:  R=1 332 -> 631,  R=2 301 -> 500,  R=3 307 -> 387, R=4 311 -> 338
     // 2D boxes: two steps per pass measured 1.26x faster per step (10240^2 fp64, radius 3)
-    // fp32 radius 1 with a working set beyond the Infinity Cache: four steps per pass
-    // (kernel_star_tbs.hip; 512^3, 10 steps: 1235 -> 1406-1471 Gpoints/s); inside it two
-    // (256^3, 10 steps: 1300 against 1230 with four)
+    // radius 1 with a working set beyond the Infinity Cache: four steps per pass in fp32,
+    // three in fp64 (kernel_star_tbs.hip; fp32 512^3, 10 steps: 1235 -> 1406-1471
+    // Gpoints/s; fp64 512^3, 9 steps: 507 -> 770-784); inside it two (fp32 256^3, 10
+    // steps: 1300 against 1230 with four)
     if (star_tbs_supported(g) && streaming_stores(g))
-        return 4;
+        return star_tbs_max_depth(g);
     if (box2_tb2_supported(g) || star_tb2_supported(g))
         return 2;
     return 1;

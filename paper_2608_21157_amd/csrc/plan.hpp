@@ -104,8 +104,9 @@ bool star_tb2_supported(const Geometry &g);
 hipError_t launch_star_tb2(const Geometry &g, const void *src, void *dst, const void *w,
                            hipStream_t stream);
 
-// Three or four star steps fused in one pass (3D, fp32, radius 1).
+// Three or four star steps fused in one pass (3D, radius 1; four in fp32, three in fp64).
 bool star_tbs_supported(const Geometry &g);
+int star_tbs_max_depth(const Geometry &g);
 hipError_t launch_star_tbs(const Geometry &g, const void *src, void *dst, const void *w,
                            int depth, hipStream_t stream);
 

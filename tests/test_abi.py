@@ -74,7 +74,7 @@ def test_status_strings_and_point_counts():
     (dict(variant=B.VARIANT_GENERIC, temporal_depth=2), B.ERR_UNSUPPORTED),
     (dict(shape=B.STAR, radius=1, temporal_depth=5), B.ERR_UNSUPPORTED),    # at most 4
     (dict(shape=B.STAR, radius=2, temporal_depth=3), B.ERR_UNSUPPORTED),    # radius 1 only
-    (dict(shape=B.STAR, radius=1, dtype=B.F64, temporal_depth=3), B.ERR_UNSUPPORTED),
+    (dict(shape=B.STAR, radius=1, dtype=B.F64, temporal_depth=4), B.ERR_UNSUPPORTED),
     (dict(dims=(1 << 11, 1 << 11, 1 << 11)), B.ERR_UNSUPPORTED),
     (dict(tile=3), B.ERR_INVALID_ARG),
     (dict(tile=-1), B.ERR_INVALID_ARG),
@@ -134,7 +134,10 @@ def test_planner_choices():
         (B.make_desc(3, (256,) * 3, shape=B.STAR, radius=1, temporal_depth=3),
          "stencil_star_tbs_kernel", 3),
         (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=1, dtype=B.F64),
+         "stencil_star_tbs_kernel", 3),
+        (B.make_desc(3, (64, 256, 256), shape=B.STAR, radius=1, dtype=B.F64),
          "stencil_star_tb2_kernel", 2),
+        (B.make_desc(3, (512,) * 3, shape=B.STAR, radius=2), "stencil_star_tb2_kernel", 2),
     ]
     for d, kernel, depth in cases:
         h = B.stencil_plan(d)

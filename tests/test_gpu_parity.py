@@ -423,24 +423,28 @@ def test_radius_zero(shape, ndim, boundary, field):
     report("radius 0 %s" % info, got, oracle_full(wl, x, w, k), tolerance(wl, x, k))
 
 
-TBS_CASES = [(d, n, bnd) for d, steps in ((4, (4, 5, 6, 7, 9)), (3, (3, 5)))
+TBS_CASES = [(dt, d, n, bnd) for dt, d, steps in (("f32", 4, (4, 5, 6, 7, 9)),
+                                                  ("f32", 3, (3, 5)), ("f64", 3, (3, 4, 5, 7)))
              for n in steps for bnd in (B.ZERO, B.PERIODIC)]
 
 
-@pytest.mark.parametrize("depth,steps,bnd", TBS_CASES,
-                         ids=["d%d-s%d-%s" % (c[0], c[1], "zero" if c[2] == B.ZERO else "per")
+@pytest.mark.parametrize("dt,depth,steps,bnd", TBS_CASES,
+                         ids=["%s-d%d-s%d-%s" % (c[0], c[1], c[2],
+                                                 "zero" if c[3] == B.ZERO else "per")
                               for c in TBS_CASES])
-def test_star_four_steps_per_pass(depth, steps, bnd):
-    """fp32 radius-1 3D stars with three or four steps fused per pass (trailing passes of
-    one or two steps for the remainder), ragged extents in every axis, every point."""
+def test_star_four_steps_per_pass(dt, depth, steps, bnd):
+    """Radius-1 3D stars with three or four steps fused per pass (fp32) or three (fp64),
+    trailing passes of one or two steps for the remainder, ragged extents in every axis,
+    every point."""
     from dataclasses import replace
     g = np.random.default_rng(200 + 10 * depth + steps)
-    for dims in ((23, 37, 72), (9, 3, 40)):
-        wl = replace(WORKLOADS["c2"].resized(dims, steps=steps), boundary=bnd)
-        x = g.uniform(-1, 1, dims).astype(np.float32)
+    npdt = np.float32 if dt == "f32" else np.float64
+    for dims in (((23, 37, 72), (9, 3, 40)) if dt == "f32" else ((21, 35, 38), (9, 3, 20))):
+        wl = replace(WORKLOADS["c2"].resized(dims, steps=steps), boundary=bnd, dtype=dt)
+        x = g.uniform(-1, 1, dims).astype(npdt)
         w = g.uniform(-1, 1, (1, wl.npoints))
-        w = (w / np.abs(w).sum()).astype(np.float32)
-        print("[case] tbs depth=%d steps=%d bnd=%d dims=%s" % (depth, steps, bnd, dims),
+        w = (w / np.abs(w).sum()).astype(npdt)
+        print("[case] tbs %s depth=%d steps=%d bnd=%d dims=%s" % (dt, depth, steps, bnd, dims),
               flush=True)
         got, info = run_library(wl, x, w, depth=depth)
         assert info["kernel"] == "stencil_star_tbs_kernel" and info["depth"] == depth, info

@@ -109,13 +109,14 @@ def test_random_description_forced_launch(seed):
 @pytest.mark.parametrize("seed", SEEDS[:60])
 def test_random_description_deepest_fusion(seed):
     """The same draws with the deepest temporal blocking the description allows (four steps
-    per pass for fp32 radius-1 3D stars, two for other 3D stars and 2D boxes)."""
+    per pass for fp32 radius-1 3D stars, three for fp64 ones, two for other 3D stars and 2D
+    boxes)."""
     wl, x, w, k = draw(seed)
     desc = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
                        dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
                        radius=wl.radius, boundary=wl.boundary, has_coeff_field=k is not None)
     depth = 1
-    for d in (4, 2):
+    for d in (4, 3, 2):
         desc.temporal_depth = d
         try:
             B.Plan(desc).close()
