@@ -370,8 +370,8 @@ bool box_stream_supported(const Geometry &g)
 hipError_t launch_box_stream(const Geometry &g, const void *src, void *dst, const void *field,
                              const void *w, hipStream_t stream)
 {
-    // 4 rows per lane (tile 1, the default: with the chunking above, 4 rows measured at
-    // least as fast as 8 on c4, c5 and c5b) or 8 (tile 2)
+    // 4 rows per lane (tile 1) or 8 (tile 2); the default depends on the coefficient
+    // field (the tile resolver states the measurements)
     const int ty = stream_tile(g, 1) == 2 ? 8 : 4;
     if (g.dtype == STENCIL_F32)
         return ty == 4 ? launch_ty<float, 4>(g, src, dst, field, w, stream)

@@ -61,10 +61,13 @@ int stream_tile(const Geometry &g, int depth)
         return 0;
     if (g.tile != 0)
         return g.tile;
-    // defaults, measured on MI355X: the 3D box runs 4 rows per lane (tile 1); the star runs
-    // 64 x 64 tiles in 3D (tile 2) and 64 x 32 tiles in 2D (tile 1)
+    // defaults, measured on MI355X: the 3D box runs 8 rows per lane (tile 2) without a
+    // coefficient field and 4 (tile 1) with one (interleaved rounds, Gpoints/s, tile 1 ->
+    // 2: depthwise 8x32x128^3 fp32 701 -> 707, 2x32x128^3 fp64 347 -> 353; 512^3 with a
+    // field 510 -> 503); the star runs 64 x 64 tiles in 3D (tile 2) and 64 x 32 tiles in
+    // 2D (tile 1)
     if (box_stream_supported(g))
-        return 1;
+        return g.field ? 1 : 2;
     return g.ndim == 3 ? 2 : 1;
 }
 

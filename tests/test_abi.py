@@ -162,9 +162,11 @@ def test_tile_and_grid_scale_choices():
     for d, tile in ((desc3(dims=(64, 64, 256), radius=4, tile=1, grid_scale=-2), 1),
                     (desc3(dims=(64, 64, 256), shape=B.BOX, tile=2, grid_scale=2), 2),
                     (desc3(dims=(8, 8, 10), grid_scale=1), 0),
-                    # 0 resolved: 4 rows per lane for the box, 64 x 64 tiles for the
-                    # one-step 3D star, 64 x 32 in 2D; the fused star has one tile
-                    (desc3(dims=(64, 64, 256), shape=B.BOX), 1),
+                    # 0 resolved: 8 rows per lane for the box (4 with a field), 64 x 64
+                    # tiles for the one-step 3D star, 64 x 32 in 2D; the fused star has
+                    # one tile
+                    (desc3(dims=(64, 64, 256), shape=B.BOX), 2),
+                    (desc3(dims=(64, 64, 256), shape=B.BOX, has_coeff_field=True), 1),
                     (desc3(dims=(64, 64, 256), radius=4, temporal_depth=1), 2),
                     (B.make_desc(2, (256, 256), radius=1), 1),
                     (desc3(dims=(64, 64, 256), radius=4), 0)):
