@@ -128,3 +128,29 @@ def test_random_description_deepest_fusion(seed):
     got, info = run_library(wl, x, w, k, depth=depth)
     report("random %d deepest %s" % (seed, info), got, oracle_full(wl, x, w, k),
            tolerance(wl, x, k))
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_random_deep_fusion(seed):
+    """Radius-1 3D stars at the deepest fusion (four steps per pass in fp32, three in fp64)
+    on drawn extents (1-30 planes, 1-45 rows, 1-20 vectors), batches with weight sets, both
+    boundaries and 1-9 steps, every point against the oracle."""
+    g = np.random.default_rng(7000 + seed)
+    dtype = str(g.choice(["f32", "f64"]))
+    vec = 4 if dtype == "f32" else 2
+    dims = (int(g.integers(1, 31)), int(g.integers(1, 46)), vec * int(g.integers(1, 21)))
+    channels = int(g.integers(1, 3))
+    batch = channels * int(g.integers(1, 3)) if g.random() < 0.4 else 1
+    wl = replace(WORKLOADS["c2"], name="deep%d" % seed, dims=dims, batch=batch,
+                 channels=channels, dtype=dtype, boundary=int(g.choice([B.ZERO, B.PERIODIC])),
+                 steps=int(g.integers(1, 10)))
+    npdt = np.float32 if dtype == "f32" else np.float64
+    x = g.uniform(-1, 1, ((batch,) if batch > 1 else ()) + dims).astype(npdt)
+    w = g.uniform(-1, 1, (channels, wl.npoints))
+    w = (w / np.abs(w).sum(axis=1, keepdims=True)).astype(npdt)
+    depth = 4 if dtype == "f32" else 3
+    print("[case] deep %d: %s bnd=%d batch=%d ch=%d steps=%d dims=%s depth=%d" % (
+        seed, dtype, wl.boundary, batch, channels, wl.steps, dims, depth), flush=True)
+    got, info = run_library(wl, x, w, depth=depth)
+    assert info["kernel"] == "stencil_star_tbs_kernel", info
+    report("deep %d %s" % (seed, info), got, oracle_full(wl, x, w), tolerance(wl, x))
