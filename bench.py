@@ -8,16 +8,26 @@ call, inputs already resident in HBM.  The metric is stencil points per second
 kernel against the compulsory-traffic roofline (each point read once and written once
 per stencil step: 8 bytes per point-step in fp32).
 
+The headline value is K back-to-back calls after W warm-up calls.  Before those, the
+headline kernel itself runs for a fixed time (``spin_up``): a stencil kernel reaches its
+steady speed only after about 20 calls of itself, whatever ran before, so the value does
+not depend on W.
+
 Prints one JSON line on stdout; progress goes to stderr.  Besides the headline (with an
-HBM roofline object and its flop-side counterpart) it reports, as context:
-  * the CPU oracle timed on a bounded slab of the headline input, and checked against
-    the GPU result there;
-  * every other workload (2D 5-point, 3D 7-point x10, 27-point box with a coefficient
-    field (periodic), depthwise 3x3x3 conv form in fp32 and fp64, and the paper's own 2D
-    radius-3 fp64 box), back to back and with the caches flushed;
-  * stencil_tune's choice and timing for each workload;
-  * a copy-probe ceiling, MIOpen's convolution on the conv-form cases, and one GPU's slab
-    of an 8-way z decomposition of the headline.
+HBM roofline object and its flop-side counterpart) it reports:
+  * per workload (2D 5-point, 3D 7-point x10, the headline, 27-point box with a
+    coefficient field (periodic), depthwise 3x3x3 conv form in fp32 and fp64, and the
+    paper's own 2D radius-3 fp64 box): back-to-back timing, and the paper's protocol --
+    3 warm-up runs, then 100 timed runs, each after the caches are flushed, graded by
+    the median, with the minimum reported;
+  * per workload, the default plan's own output checked against the fp64 CPU oracle at
+    every point of the full-size grid (the oracle's wall time, threads and error);
+  * the oracle timed single-threaded on a bounded slab of the headline input
+    (``cpu_baseline``);
+  * stencil_tune's choice and timing for each workload, a copy-probe ceiling, MIOpen's
+    convolution on the paper and conv-form cases, and one GPU's slab of an 8-way z
+    decomposition of the headline (context).
+All GPU work runs before the CPU legs, so host threads never overlap a timed region.
 Every reported value is the planner's default plan.
 """
 from __future__ import annotations
@@ -122,16 +132,16 @@ def counter_traffic(kernel: str, workload: str, algo_bytes: float):
 class Runner:
     def __init__(self, torch, B, inputs, wl, stream, depth=0):
         self.torch, self.B, self.wl, self.stream = torch, B, wl, stream
-        import numpy as np
         t0 = time.perf_counter()
         x, w, k = inputs.make(wl)
         log("[bench] %s: inputs generated in %.1fs" % (wl.name, time.perf_counter() - t0))
-        self.x_host = x
+        self.x_host, self.k_host = x, k
         dev = torch.device("cuda:0")
         self.x = torch.from_numpy(x).to(dev)
         self.y = torch.empty_like(self.x)
         self.k = None if k is None else torch.from_numpy(k).to(dev)
         self.w = np.ascontiguousarray(w)
+        torch.cuda.synchronize()  # the uploads ran on torch's stream; the calls use `stream`
         desc = B.make_desc(wl.ndim, wl.dims, batch=wl.batch, channels=wl.channels,
                            dtype=B.F32 if wl.dtype == "f32" else B.F64, shape=wl.shape,
                            radius=wl.radius, boundary=wl.boundary,
@@ -140,12 +150,26 @@ class Runner:
         info = self.plan.info()
         self.kernel = info.kernel.decode()
         self.depth = info.temporal_depth
+        self.tile, self.grid_scale = info.tile, info.grid_scale
         self.variant = B.VARIANT_NAMES.get(info.variant, str(info.variant))
         self.launches = math.ceil(wl.steps / self.depth) if wl.steps else 0
 
-    def call(self):
-        self.plan.run(self.x, self.y, self.w, steps=self.wl.steps, field=self.k,
-                      stream=self.stream)
+    def call(self, steps=None):
+        self.plan.run(self.x, self.y, self.w, steps=self.wl.steps if steps is None else steps,
+                      field=self.k, stream=self.stream)
+
+    def spin(self, seconds: float) -> int:
+        """Calls of this workload itself, back to back, for `seconds` (untimed): the
+        kernel's steady speed is reached after about 20 calls of itself."""
+        t0 = time.perf_counter()
+        n = 0
+        while True:
+            for _ in range(5):
+                self.call()
+            n += 5
+            self.stream.synchronize()
+            if time.perf_counter() - t0 >= seconds:
+                return n
 
     def timed(self, K: int, W: int) -> float:
         """Milliseconds for K back-to-back calls (events on the launch stream)."""
@@ -194,14 +218,17 @@ class Runner:
     def call_on(self, stream):
         self.plan.run(self.x, self.y, self.w, steps=self.wl.steps, field=self.k, stream=stream)
 
-    def flushed(self, R: int, flush) -> list:
-        """Per-call milliseconds with L2 and the Infinity Cache flushed before each call
-        (the flush runs on the same stream, outside the events)."""
+    def flushed(self, R: int, flush, warm: int = 3) -> list:
+        """The paper's protocol: `warm` untimed calls, then R calls timed one by one
+        (events on the launch stream), each after `flush` has evicted the caches on the
+        same stream, outside the events.  Returns the R per-call milliseconds."""
         torch = self.torch
+        for _ in range(warm):
+            self.call()
+        self.stream.synchronize()
         out = []
         for i in range(R):
-            with torch.cuda.stream(self.stream):  # ordered before the events, not beside them
-                flush.fill_(float(i))
+            flush(self.stream, i)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(self.stream)
@@ -211,9 +238,68 @@ class Runner:
             out.append(e0.elapsed_time(e1))
         return out
 
+    def output(self) -> np.ndarray:
+        """Host copy of `out` after the work queued so far."""
+        self.stream.synchronize()
+        return self.y.cpu().numpy()
+
     def close(self):
         self.plan.close()
         del self.x, self.y, self.k
+
+
+class Flush:
+    """Evicts L2 and the Infinity Cache by reading a 1 GiB buffer on a given stream.
+    Reading (a sum) rather than writing leaves only clean lines behind: the dirty lines
+    of the previous call are written back during the flush, and the timed call does not
+    pay to write back the flush's own data."""
+
+    def __init__(self, torch, nbytes: int = 1 << 30):
+        self.torch = torch
+        self.buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        torch.cuda.synchronize()
+
+    def __call__(self, stream, i: int) -> None:
+        with self.torch.cuda.stream(stream):
+            self.sink = self.buf.sum()
+
+
+def protocol_record(wl, times: list) -> dict:
+    med = statistics.median(times)
+    return {"calls": len(times), "warmup": 3, "flush": "1 GiB read on the timed stream",
+            "median_ms": round(med, 5), "min_ms": round(min(times), 5),
+            "gpoints_per_s_median": figures(wl, med)["gpoints_per_s"],
+            "gpoints_per_s_min_time": figures(wl, min(times))["gpoints_per_s"],
+            "frac_of_8tbs_median": figures(wl, med)["frac_of_8tbs"]}
+
+
+def tolerance(wl, x, k=None) -> float:
+    """The parity bar: fp32 1e-5 per step, scaled by max|x| (and max k) above 1; fp64 a
+    flat 1e-12."""
+    if wl.dtype != "f32":
+        return 1e-12
+    scale = max(1.0, float(np.abs(x).max()))
+    if k is not None:
+        scale *= max(1.0, float(np.abs(k).max()))
+    return 1e-5 * max(wl.steps, 1) * scale
+
+
+def oracle_check(wl, x, w, k, got, what: str) -> dict:
+    """`got` against the fp64 oracle at every point of the grid (the oracle evaluated in
+    independent slabs or volumes on host threads; see oracle/whole_grid.py)."""
+    from oracle import whole_grid
+    rep = whole_grid.compare(got, x, w, shape=wl.shape, radius=wl.radius,
+                             boundary=wl.boundary, steps=wl.steps, ndim=wl.ndim,
+                             channels=wl.channels, field=k)
+    tol = tolerance(wl, x, k)
+    pts = int(x.size) * max(wl.steps, 1)
+    ok = rep["nonfinite"] == 0 and rep["max_abs_err"] <= tol
+    return {"what": what, "points": rep["points"], "steps": wl.steps,
+            "max_abs_err": rep["max_abs_err"], "worst_flat_index": rep["worst"],
+            "nonfinite": rep["nonfinite"], "tolerance": tol, "pass": bool(ok),
+            "oracle_seconds": rep["seconds"], "oracle_threads": rep["threads"],
+            "oracle_pieces": rep["pieces"],
+            "oracle_gpoints_per_s": round(pts / max(rep["seconds"], 1e-9) / 1e9, 5)}
 
 
 def figures(wl, ms_per_call: float) -> dict:
@@ -346,7 +432,7 @@ def slab_context(torch, B, inputs, stream, gpus=8, reps=20) -> dict:
     halo = 2 * wl.radius  # planes per side for two fused steps
     slab = wl.resized((own + 2 * halo,) + tuple(wl.dims[1:]), steps=2)
     r = Runner(torch, B, inputs, slab, stream)
-    spin_up(torch, stream, 0.1)
+    r.spin(0.3)
     t = r.timed(reps, 3) / reps
     kernel = r.kernel
     r.close()
@@ -367,7 +453,7 @@ def deep_fusion_context(torch, B, inputs, stream, reps=20) -> dict:
     out = {"dims": list(wl.dims), "steps": wl.steps}
     for key, depth in (("planner", 0), ("two_per_pass", 2)):
         r = Runner(torch, B, inputs, wl, stream, depth=depth)
-        spin_up(torch, stream, 0.1)
+        r.spin(0.3)
         t = r.timed(reps, 10) / reps
         out[key] = {"kernel": r.kernel, "depth": r.depth, "ms_per_call": round(t, 5),
                     "gpoints_per_s": figures(wl, t)["gpoints_per_s"]}
@@ -437,52 +523,55 @@ def host_info(torch) -> dict:
     return info
 
 
-def cpu_baseline(wl, x_host, w, planes: int, y_gpu=None):
-    """The fp64 oracle, single-threaded, on a z-slab of the headline input.  With the
-    GPU's result `y_gpu` (the same leading planes, zero boundary), the slab's planes
-    below z = planes - R * steps -- those the cut face cannot reach in `steps` steps --
-    are also compared with it point by point."""
+def cpu_baseline(wl, x_host, w, planes: int):
+    """The fp64 oracle as it stands, single-threaded, on a z-slab of the headline input:
+    the CPU reference throughput (a reported baseline, not a target)."""
     import oracle
     oracle.build()
     slab = x_host[:planes]
     t0 = time.perf_counter()
-    ref = oracle.apply(slab, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
-                       steps=wl.steps, ndim=wl.ndim)
+    oracle.apply(slab, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                 steps=wl.steps, ndim=wl.ndim)
     dt = time.perf_counter() - t0
     pts = slab.size * wl.steps
-    out = {"value": round(pts / dt / 1e9, 6), "unit": "Gpoints/s", "cores": 1,
-           "kind": "oracle", "seconds": round(dt, 2),
-           "sample": "%dx%dx%d z-slab of the headline input, %d steps, fp64 single thread"
-                     % (slab.shape + (wl.steps,))}
-    valid = planes - wl.radius * wl.steps
-    if y_gpu is not None and wl.boundary == 0 and valid > 0:
-        err = float(np.abs(ref[:valid] - y_gpu[:valid].astype(np.float64)).max())
-        base = 1e-5 if wl.dtype == "f32" else 1e-12
-        tol = base * max(wl.steps, 1) * max(1.0, float(np.abs(slab).max()))
-        out["check"] = {"planes": valid, "points": int(ref[:valid].size),
-                        "max_abs_err": err, "tolerance": tol, "pass": bool(err <= tol)}
-    return out
+    return {"value": round(pts / dt / 1e9, 6), "unit": "Gpoints/s", "cores": 1,
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": "%dx%dx%d z-slab of the headline input, %d steps, fp64 single thread"
+                      % (slab.shape + (wl.steps,))}
+
+
+# workloads of the per-workload block, in order; the headline's own record is reused for
+# its name rather than timed twice
+WORKLOAD_ORDER = ("c1", "c2", "c3", "c4", "c5", "c5b", "paper")
+PROTOCOL_CALLS = 100
+# the paper workload's output is checked on a call of 4 steps (two fused launches through
+# the ping-pong grid, in the timed launch configuration): its timed 256-step call is
+# beyond a whole-grid oracle's reach
+PAPER_CHECK_STEPS = 4
 
 
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    # 30 untimed calls by default: after other work (or none), the stencil kernels reach
-    # their steady speed only after ~20 calls (measured on c3: 657 -> 755 -> 769 Gpoints/s
-    # over the first three 20-call blocks)
     ap.add_argument("--steps", type=int, default=50, help="timed calls")
     ap.add_argument("--warmup", type=int, default=30, help="untimed calls")
+    ap.add_argument("--spin-s", type=float, default=0.3,
+                    help="seconds of untimed calls of the headline kernel before the warm-up")
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-checks", action="store_true",
+                    help="skip the whole-grid oracle checks of the outputs")
+    ap.add_argument("--protocol-calls", type=int, default=PROTOCOL_CALLS,
+                    help="flushed, individually timed calls per workload (0: none)")
     ap.add_argument("--no-others", action="store_true", help="headline workload only")
     ap.add_argument("--cpu-planes", type=int, default=320,
-                    help="z planes of the headline input the CPU oracle runs on (~10-20 s)")
+                    help="z planes of the headline input the single-thread oracle runs on")
     ap.add_argument("--stencil-steps", type=int, default=0,
                     help="override the workload's stencil steps per call (profiling runs)")
     ap.add_argument("--depth", type=int, default=0,
                     help="stencil steps fused per launch (0: the planner's choice)")
     ap.add_argument("--no-tune", action="store_true",
-                    help="skip the stencil_tune context figure of the headline workload")
+                    help="skip the stencil_tune context figures")
     ap.add_argument("--copy-only", action="store_true",
                     help="run only the copy probe (counter calibration runs)")
     args = ap.parse_args()
@@ -509,9 +598,14 @@ def main() -> int:
     wl = inputs.WORKLOADS[args.workload]
     if args.stencil_steps > 0:
         wl = wl.resized(wl.dims, steps=args.stencil_steps)
+    flush = Flush(torch) if args.protocol_calls > 0 else None
+    checks_todo = []   # (name, workload, x, w, k, output, what): run after all GPU work
 
+    # ---- headline: spin-up on its own kernel, W warm-up calls, K timed calls ------------
     head = Runner(torch, B, inputs, wl, stream, depth=args.depth)
-    spun = spin_up(torch, stream)
+    t0 = time.perf_counter()
+    spin_calls = head.spin(args.spin_s) if args.spin_s > 0 else 0
+    spun = round(time.perf_counter() - t0, 3)
     ms_total = head.timed(args.steps, args.warmup)
     ms = ms_total / args.steps
     fig = figures(wl, ms)
@@ -525,29 +619,44 @@ def main() -> int:
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "kernel": head.kernel,
                 "avg_launch_ms": round(avg_launch_ms, 5),
-                "algorithmic_bytes_per_launch": int(algo_per_launch)}
+                "algorithmic_bytes_per_launch": int(algo_per_launch),
+                "achieved_is": "sweep-compulsory bytes (each fused step's read and write) "
+                               "per launch over the event-timed launch time",
+                "counter_gbs": (round(traffic / (avg_launch_ms * 1e-3) / 1e9, 1)
+                                if traffic else None)}
     roofline_alu = alu_roofline(wl, head.launches, avg_launch_ms)
-    log("[bench] %s: %.4f ms/call, %.1f Gpoints/s, %.1f GB/s (%.1f%% of 8 TB/s)" % (
-        wl.name, ms, fig["gpoints_per_s"], achieved, 100 * achieved / HBM_PEAK_GBS))
+    log("[bench] %s: %.4f ms/call, %.1f Gpoints/s, %.1f GB/s (%.1f%% of 8 TB/s); spin-up "
+        "%d calls" % (wl.name, ms, fig["gpoints_per_s"], achieved, 100 * achieved / HBM_PEAK_GBS,
+                      spin_calls))
+    head_rec = dict(fig)
+    head_rec.update(kernel=head.kernel, variant=head.variant, depth=head.depth,
+                    tile=head.tile, grid_scale=head.grid_scale,
+                    launches_per_call=head.launches, timed_calls=args.steps)
+    if not args.no_checks:
+        # the timed default plan's own output, before anything else writes `out`
+        checks_todo.append((wl.name, wl, head.x_host, head.w, head.k_host, head.output(),
+                            "the timed default plan's output"))
+    protocol = None
+    if flush is not None:
+        protocol = protocol_record(wl, head.flushed(args.protocol_calls, flush))
+        head_rec["protocol"] = protocol
+        log("[bench] %s protocol: %s" % (wl.name, protocol))
 
     tuned = None
     if not args.no_tune:
         tuned = tune_context(torch, B, head, args.steps, args.warmup)
+        head_rec["tuned"] = {k: tuned[k] for k in ("chosen", "kernel", "candidates", "valid",
+                                                    "ms_per_call", "gpoints_per_s")}
         log("[bench] tuned %s: %s" % (wl.name, tuned))
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        planes = min(args.cpu_planes, wl.dims[0])
-        y_gpu = head.y[:planes].cpu().numpy() if wl.ndim == 3 and wl.batch == 1 else None
-        cpu = cpu_baseline(wl, head.x_host, head.w, planes, y_gpu)
-        log("[bench] cpu oracle: %s" % cpu)
+    cpu_input = (head.x_host, head.w) if (not args.no_cpu_baseline and wl.ndim == 3
+                                          and wl.batch == 1) else None
     head.close()
     torch.cuda.empty_cache()
 
     others = {}
     probe = None
     if not args.no_others:
-        spin_up(torch, stream)  # the GPU idled during the CPU leg
+        spin_up(torch, stream)
         probe = copy_probe(torch, stream)
         log("[bench] copy probe: %s" % probe)
         patterns = {}
@@ -557,74 +666,66 @@ def main() -> int:
                 patterns[key] = copy_probe(torch, stream, nbytes, kind=kind)
                 log("[bench] %s probe, %d MiB per array: %s" % (kind, nbytes >> 20,
                                                                  patterns[key]))
-        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0")  # 1 GiB
-        for name in ("c1", "c2", "c3", "c4", "c5", "c5b", "paper"):
-            w2 = inputs.WORKLOADS[name]
-            if name == "paper":
-                # the paper iterates 10,240 times and reports the amortised per-step
-                # latency; 256-step calls amortise the same way at a tenth of the time
-                w2 = w2.resized(w2.dims, steps=PAPER_STEPS_TIMED)
-            r = Runner(torch, B, inputs, w2, stream)
-            spin_up(torch, stream, 0.1)  # host-side input generation left the GPU idle
-            # warm-up: a kernel reaches its steady speed after about 20 calls of itself
-            reps = 3 if name == "paper" else 20
-            t = r.timed(reps, 1 if name == "paper" else 20) / reps
-            fl = r.flushed(2 if name == "paper" else 10, flush)
-            rec = figures(w2, t)
-            rec["flushed_median_ms"] = round(statistics.median(fl), 5)
-            rec["flushed_min_ms"] = round(min(fl), 5)
-            rec["flushed_gpoints_per_s"] = figures(w2, statistics.median(fl))["gpoints_per_s"]
-            rec.update(kernel=r.kernel, variant=r.variant, depth=r.depth,
-                       launches_per_call=r.launches)
+        for name in WORKLOAD_ORDER:
+            if name == wl.name:
+                rec = head_rec
+            else:
+                w2 = inputs.WORKLOADS[name]
+                if name == "paper":
+                    # the paper iterates 10,240 times and reports the amortised per-step
+                    # latency; 256-step calls amortise the same way at a tenth of the time
+                    w2 = w2.resized(w2.dims, steps=PAPER_STEPS_TIMED)
+                rec = workload_leg(torch, B, inputs, w2, stream, flush, args, checks_todo)
             if probe:
                 rec["frac_of_copy_probe"] = round(rec["effective_gbs"] / probe["gbs"], 4)
             if name in PATTERN_PROBES:
                 pp = patterns[PATTERN_PROBES[name]]
                 rec["pattern_probe"] = pp
                 rec["frac_of_pattern_probe"] = round(rec["effective_gbs"] / pp["gbs"], 4)
-            if not args.no_tune:
-                # the fastest valid launch configuration for this workload (the tuner's
-                # search), timed like the default plan above
-                tr = tune_context(torch, B, r, reps, 1 if name == "paper" else 3,
-                                  reps=3 if name == "paper" else 5)
-                rec["tuned"] = {k: tr[k] for k in ("chosen", "kernel", "candidates", "valid",
-                                                   "ms_per_call", "gpoints_per_s")}
-            if name in ("c1", "c2"):
-                # launch-bound workloads: the same calls replayed from a HIP graph
-                gms = r.graph_timed(50, 20)
-                rec["graph_replay"] = {"ms_per_call": round(gms, 5),
-                                       "gpoints_per_s": figures(w2, gms)["gpoints_per_s"],
-                                       "calls_per_graph": 50}
-            if name == "paper":
-                rec["ms_per_stencil_step"] = round(t / w2.steps, 5)
-                rec["context_a100_ms_per_step"] = PAPER_A100_MS_PER_STEP
-            if name in ("paper", "c5"):
-                rec["context_miopen"] = miopen_context(torch, w2, r.x_host, r.w)
             others[name] = rec
             log("[bench] %s: %s" % (name, rec))
-            r.close()
-            torch.cuda.empty_cache()
         others["c3_slab_of_8"] = slab_context(torch, B, inputs, stream)
         log("[bench] c3_slab_of_8: %s" % others["c3_slab_of_8"])
         others["c2_at_512_cubed"] = deep_fusion_context(torch, B, inputs, stream)
         log("[bench] c2_at_512_cubed: %s" % others["c2_at_512_cubed"])
-        del flush
+    del flush
+    torch.cuda.empty_cache()
+
+    # ---- CPU legs, after every GPU measurement -----------------------------------------
+    cpu = None
+    if cpu_input is not None:
+        planes = min(args.cpu_planes, wl.dims[0])
+        cpu = cpu_baseline(wl, cpu_input[0], cpu_input[1], planes)
+        log("[bench] cpu oracle: %s" % cpu)
+    checks = {}
+    for name, cwl, x, w, k, got, what in checks_todo:
+        checks[name] = oracle_check(cwl, x, w, k, got, what)
+        log("[bench] oracle check %s: %s" % (name, checks[name]))
+        if name in others:
+            others[name]["oracle_check"] = checks[name]
+        del got
+    checks_todo.clear()
 
     line = {
         "metric": "stencil Gpoints/s and achieved HBM GB/s (% of MI355X peak), 3D fp32 512^3",
         "value": fig["gpoints_per_s"], "unit": "Gpoints/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "spin_up_s": spun,
+        "steps": args.steps, "warmup": args.warmup,
+        "spin_up": {"seconds": spun, "calls": spin_calls,
+                    "what": "untimed calls of the headline workload before the warm-up"},
         "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic, seeded: " + DATA[wl.recipe],
         "config": {"workload": describe(wl),
                    "dims": list(wl.dims), "stencil_steps_per_call": wl.steps,
-                   "kernel": head.kernel, "variant": head.variant,
-                   "temporal_depth": head.depth, "parallelism": "single GPU"},
+                   "kernel": head_rec["kernel"], "variant": head_rec["variant"],
+                   "temporal_depth": head_rec["depth"], "parallelism": "single GPU"},
         "effective_gbs": fig["effective_gbs"],
         "run_compulsory_gbs": fig["run_compulsory_gbs"],
         "roofline": roofline,
         "roofline_alu": roofline_alu,
+        "protocol": protocol,
+        "oracle_check": checks.get(wl.name),
+        "oracle_checks_pass": (all(c["pass"] for c in checks.values()) if checks else None),
         "tuned": tuned,
         "host": host_info(torch),
         "cpu_baseline": cpu,
@@ -633,6 +734,51 @@ def main() -> int:
     }
     print(json.dumps(line), flush=True)
     return 0
+
+
+def workload_leg(torch, B, inputs, wl, stream, flush, args, checks_todo) -> dict:
+    """One workload of the per-workload block: spin-up on its own kernel, 20 back-to-back
+    calls after 20 warm-up calls, the flushed protocol, the tuner's choice, and (queued
+    for the CPU phase) its output for the whole-grid oracle check."""
+    r = Runner(torch, B, inputs, wl, stream)
+    paper = wl.name == "paper"
+    r.spin(0.3)
+    reps = 3 if paper else 20
+    t = r.timed(reps, 1 if paper else 20) / reps
+    rec = figures(wl, t)
+    rec.update(kernel=r.kernel, variant=r.variant, depth=r.depth, tile=r.tile,
+               grid_scale=r.grid_scale, launches_per_call=r.launches, timed_calls=reps)
+    if not args.no_checks:
+        if paper:
+            r.call(steps=PAPER_CHECK_STEPS)
+            checks_todo.append((wl.name, wl.resized(wl.dims, steps=PAPER_CHECK_STEPS),
+                                r.x_host, r.w, r.k_host, r.output(),
+                                "a %d-step call of the timed default plan" % PAPER_CHECK_STEPS))
+        else:
+            checks_todo.append((wl.name, wl, r.x_host, r.w, r.k_host, r.output(),
+                                "the timed default plan's output"))
+    if flush is not None:
+        rec["protocol"] = protocol_record(wl, r.flushed(args.protocol_calls, flush))
+    if not args.no_tune:
+        # the fastest valid launch configuration for this workload (the tuner's search),
+        # timed like the default plan above
+        tr = tune_context(torch, B, r, reps, 1 if paper else 3, reps=3 if paper else 5)
+        rec["tuned"] = {k: tr[k] for k in ("chosen", "kernel", "candidates", "valid",
+                                           "ms_per_call", "gpoints_per_s")}
+    if wl.name in ("c1", "c2"):
+        # launch-bound workloads: the same calls replayed from a HIP graph
+        gms = r.graph_timed(50, 20)
+        rec["graph_replay"] = {"ms_per_call": round(gms, 5),
+                               "gpoints_per_s": figures(wl, gms)["gpoints_per_s"],
+                               "calls_per_graph": 50}
+    if paper:
+        rec["ms_per_stencil_step"] = round(t / wl.steps, 5)
+        rec["context_a100_ms_per_step"] = PAPER_A100_MS_PER_STEP
+    if wl.name in ("paper", "c5"):
+        rec["context_miopen"] = miopen_context(torch, wl, r.x_host, r.w)
+    r.close()
+    torch.cuda.empty_cache()
+    return rec
 
 
 if __name__ == "__main__":

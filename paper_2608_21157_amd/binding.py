@@ -65,6 +65,7 @@ class StencilError(RuntimeError):
 
 
 _lib = None
+_raw_apply = None   # stencil_apply without argtypes, for Plan.run's pre-built arguments
 
 
 def load():
@@ -96,6 +97,11 @@ def load():
                                  ctypes.c_int32, ctypes.c_double, ctypes.c_int32, vp,
                                  ctypes.POINTER(StencilTuneReport)]
     lib.stencil_tune.restype = ctypes.c_int
+    global _raw_apply
+    # a second handle of the same library, so that this function object has no argtypes:
+    # Plan.run passes ctypes objects only, and the call then converts nothing
+    _raw_apply = ctypes.CDLL(LIB_PATH).stencil_apply
+    _raw_apply.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -178,32 +184,101 @@ def make_desc(ndim, dims, *, batch=1, channels=1, dtype=F32, shape=STAR, radius=
 
 
 class Plan:
-    """Owns a ``stencil_plan_t``; ``run`` calls ``stencil_apply`` on torch tensors."""
+    """Owns a ``stencil_plan_t``; ``run`` calls ``stencil_apply`` on torch tensors.
+
+    ``run`` validates its tensors and weight array once per new object: the dtype is the
+    plan's, the element count is batch * volume, tensors are contiguous CUDA tensors on
+    one device, and the weights are a C-contiguous numpy array of channels * npoints
+    values of the plan's dtype.  A failed check raises ``ValueError`` before the library
+    is called.  The objects last validated are held until another one is passed (or the
+    plan is closed), so an unchanged object is not checked again; resizing a validated
+    tensor in place between calls is not detected.  Weight values changed in place are
+    still seen: the library compares the weights' bytes on every call."""
 
     def __init__(self, desc: StencilDesc):
         self.desc = desc
         self.handle = stencil_plan(desc)
         self.dims = tuple(desc.dims[i] for i in range(desc.ndim))
         self._dims_c = _dims3(self.dims)  # built once: run() is on the latency path
-        self._coeffs = (None, None)       # last weight array and its host address
-        self._stream = None
+        self._numel = int(desc.batch)
+        for d in self.dims:
+            self._numel *= int(d)
+        self._ncoeffs = int(desc.channels) * stencil_num_points(desc.shape, desc.ndim,
+                                                                desc.radius)
+        self._stream = None               # last stream run on (close() waits for it)
+        self._seen = (None, None, None, None)   # x, y, field, coeffs last validated
+        self._sh_obj = None               # stream object whose handle is in _sh
+        # pre-built arguments of the raw call (no per-call ctypes conversion)
+        vp = ctypes.c_void_p
+        self._raw = _raw_apply
+        self._h = vp(self.handle)
+        self._pin, self._pout, self._pfield, self._pc, self._sh = vp(), vp(), vp(), vp(), vp()
+        self._radius_c = ctypes.c_int32(desc.radius)
+        self._bnd_c = ctypes.c_int32(desc.boundary)
+        self._steps_c = ctypes.c_int32(0)
 
     def info(self) -> StencilPlanInfo:
         return stencil_plan_query(self.handle)
 
-    def run(self, x, y, coeffs, *, steps: int, field=None, stream=None) -> None:
+    def _validate(self, x, y, coeffs, field) -> None:
+        import numpy as np
         import torch
+        want = torch.float32 if self.desc.dtype == F32 else torch.float64
+        named = [("x", x), ("y", y)] + ([("field", field)] if field is not None else [])
+        for name, t in named:
+            if not isinstance(t, torch.Tensor):
+                raise ValueError("%s must be a torch tensor" % name)
+            if t.dtype != want:
+                raise ValueError("%s has dtype %s, the plan computes in %s" % (name, t.dtype,
+                                                                              want))
+            if t.numel() != self._numel:
+                raise ValueError("%s has %d elements, the plan needs batch * volume = %d"
+                                 % (name, t.numel(), self._numel))
+            if not t.is_contiguous():
+                raise ValueError("%s must be contiguous" % name)
+        if (field is not None) != bool(self.desc.has_coeff_field):
+            raise ValueError("the plan needs a coefficient field" if self.desc.has_coeff_field
+                             else "the plan has no coefficient field")
+        npdt = np.float32 if self.desc.dtype == F32 else np.float64
+        if not isinstance(coeffs, np.ndarray):
+            raise ValueError("coeffs must be a numpy array on the host")
+        if coeffs.dtype != npdt:
+            raise ValueError("coeffs has dtype %s, the plan computes in %s" % (
+                coeffs.dtype, np.dtype(npdt)))
+        if coeffs.size != self._ncoeffs:
+            raise ValueError("coeffs has %d values, the plan needs channels * npoints = %d"
+                             % (coeffs.size, self._ncoeffs))
+        if not coeffs.flags.c_contiguous:
+            raise ValueError("coeffs must be C-contiguous")
+        devs = {t.device for _, t in named}
+        if any(d.type != "cuda" for d in devs) or len(devs) != 1:
+            raise ValueError("x, y (and field) must be CUDA tensors on one device")
+        self._seen = (x, y, field, coeffs)
+        self._pc.value = coeffs.ctypes.data
+
+    def run(self, x, y, coeffs, *, steps: int, field=None, stream=None) -> None:
+        seen = self._seen
+        if x is not seen[0] or y is not seen[1] or field is not seen[2] or coeffs is not seen[3]:
+            self._validate(x, y, coeffs, field)
         if stream is None:
+            import torch
             stream = torch.cuda.current_stream()
-        sh = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+        if stream is not self._sh_obj:
+            self._sh.value = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+            self._sh_obj = stream
         self._stream = stream
-        # the same array object keeps its buffer; the library compares the weights' bytes
-        # on every call, so values changed in place are still uploaded
-        if self._coeffs[0] is not coeffs:
-            self._coeffs = (coeffs, coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs)
-        stencil_apply(self.handle, x.data_ptr(), y.data_ptr(), self._dims_c, self._coeffs[1],
-                      None if field is None else field.data_ptr(), self.desc.radius,
-                      self.desc.boundary, steps, sh)
+        self._pin.value = x.data_ptr()
+        self._pout.value = y.data_ptr()
+        pf = None
+        if field is not None:
+            self._pfield.value = field.data_ptr()
+            pf = self._pfield
+        if self._steps_c.value != steps:
+            self._steps_c.value = steps
+        st = self._raw(self._h, self._pin, self._pout, self._dims_c, self._pc, pf,
+                       self._radius_c, self._bnd_c, self._steps_c, self._sh)
+        if st != OK:
+            _check(st)
 
     def tune(self, x, y, coeffs, *, steps: int, field=None, tolerance: float = -1.0,
              reps: int = 0, stream=None) -> dict:
@@ -211,6 +286,7 @@ class Plan:
         validity gate in this plan and leaves its result in ``y``.  Returns the report as
         a dict: ``tolerance``, ``chosen`` (index) and ``candidates`` (list of dicts)."""
         import torch
+        self._validate(x, y, coeffs, field)
         if stream is None:
             stream = torch.cuda.current_stream()
         sh = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
@@ -228,12 +304,14 @@ class Plan:
 
     def close(self) -> None:
         """Wait for the last stream this plan ran on, then free the plan."""
-        self._coeffs = (None, None)
+        self._seen = (None, None, None, None)
+        self._sh_obj = None
         if self.handle:
             if self._stream is not None and hasattr(self._stream, "synchronize"):
                 self._stream.synchronize()
             stencil_destroy(self.handle)
             self.handle = None
+            self._h.value = None
 
     def __del__(self):
         try:

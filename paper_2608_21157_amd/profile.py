@@ -18,8 +18,14 @@ size, which the copy calibration shows as a factor of 2.
 Each counter pass asks for one counter group only: rocprofv3 does not split counters
 over passes, and one request beyond a block's counter slots stalls it.  Every pass runs
 under a hard time limit (SIGKILL), from /tmp with TMPDIR=/tmp, with the program itself
-after ``--``.  A pass that ends with a non-zero status after writing complete results is
-accepted: rocprofv3 can fault in its own teardown after the program has finished.
+after ``--``.  Every pass's exit status and wall time are written to
+``OUT/pass_status.json`` and repeated in each summary.  A pass that ends with a non-zero
+status after writing complete results is kept, and its status is recorded beside its
+figures (rocprofv3 can fault in its own teardown after the program has finished); a
+pass killed at its limit, or one that left no results, stops the run.  The counter
+passes run the bench with few calls (one warm-up and one timed call, no spin-up): each
+counter-collected dispatch is serialised, so a pass over thousands of dispatches (the
+paper workload's 10,240-step calls once were) does not finish in its limit.
 
 ``--write`` turns the raw outputs in OUT into the summaries under ``profiles/``: one
 text file per kernel and workload, giving the commands, the kernel statistics and the
@@ -75,8 +81,12 @@ def occupancy(wave_cycles: float, busy_cycles: float) -> float:
 
 
 def bench_args(workload: str, timed: bool) -> list:
-    """bench.py arguments of one pass: the headline leg only, no tuner, no CPU leg."""
-    args = ["--no-others", "--no-cpu-baseline", "--no-tune", "--workload", workload]
+    """bench.py arguments of one pass: the headline leg only, no tuner, no CPU leg, no
+    oracle check and no flushed protocol; the counter passes without the spin-up."""
+    args = ["--no-others", "--no-cpu-baseline", "--no-tune", "--no-checks",
+            "--protocol-calls", "0", "--workload", workload]
+    if not timed:
+        args += ["--spin-s", "0"]
     if workload == "paper":
         args += ["--stencil-steps", str(PAPER_STEPS)]
         args += ["--steps", "3", "--warmup", "1"] if timed else ["--steps", "1", "--warmup", "1"]
@@ -104,8 +114,24 @@ def command(opts, name, workload, args, out="OUT", bench="R/bench.py") -> list:
                                     "-o", workload, "--", "python3", bench] + args)
 
 
+STATUS_FILE = "pass_status.json"
+
+
+def record_status(out: str, name: str, rec: dict) -> None:
+    path = os.path.join(out, STATUS_FILE)
+    data = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            data = json.load(f)
+    data[name] = rec
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+
+
 def run_passes(out: str, workloads) -> None:
-    """Run every pass of the workloads (and of the copy probe); stop at the first failure."""
+    """Run every pass of the workloads (and of the copy probe); stop at the first pass
+    killed at its limit or left without results.  Each pass's status is recorded."""
+    import time
     env = dict(os.environ, TMPDIR="/tmp")
     for w in list(workloads) + ["copy"]:
         for name, opts, args, limit in passes(w):
@@ -113,15 +139,24 @@ def run_passes(out: str, workloads) -> None:
             cmd[cmd.index("python3")] = sys.executable
             print("== %s" % name, flush=True)
             log = open(os.path.join(out, name + ".log"), "w")
+            t0 = time.time()
             try:
                 r = subprocess.run(cmd, cwd="/tmp", env=env, stdout=log, stderr=subprocess.STDOUT,
                                    timeout=limit)
                 status = r.returncode
             except subprocess.TimeoutExpired:
+                record_status(out, name, {"status": "killed at the %d s limit" % limit,
+                                          "seconds": round(time.time() - t0, 1),
+                                          "complete": False})
                 raise SystemExit("%s: killed at its %d s limit" % (name, limit))
             finally:
                 log.close()
-            if status != 0 and not results_complete(out, name, w):
+            complete = results_complete(out, name, w)
+            record_status(out, name, {"status": status, "seconds": round(time.time() - t0, 1),
+                                      "complete": complete})
+            print("   exit status %d, results %s" % (status, "complete" if complete else
+                                                      "missing"), flush=True)
+            if status != 0 and not complete:
                 raise SystemExit("%s: rocprofv3 exited with %d (see %s.log)" % (name, status, name))
 
 
@@ -157,11 +192,31 @@ def copy_calibration(out: str) -> tuple:
     return COPY_BYTES / (fetch * 1024), COPY_BYTES / (write * 1024), fetch, write
 
 
-def fmt_cmds(workload: str) -> str:
+def pass_statuses(out: str) -> dict:
+    path = os.path.join(out, STATUS_FILE)
+    if not os.path.exists(path):
+        return {}
+    with open(path) as f:
+        return json.load(f)
+
+
+def fmt_cmds(workload: str, statuses: dict | None = None) -> str:
     lines = ["# commands (run from /tmp with TMPDIR=/tmp; R = repository root; or all of them"
              " through `python -m paper_2608_21157_amd.profile --out OUT --write`):"]
     for name, opts, args, _ in passes(workload):
         lines.append("#   " + " ".join(command(opts, name, workload, args)))
+    if statuses is not None:
+        parts = []
+        for name, _, _, _ in passes(workload):
+            st = statuses.get(name)
+            parts.append("%s %s" % (name, "not recorded" if st is None else
+                                    "%s (%.0f s)" % (st["status"], st.get("seconds", 0))))
+        lines.append("# exit status of each pass: " + ", ".join(parts))
+        bad = [n for n, _, _, _ in passes(workload)
+               if statuses.get(n) and statuses[n]["status"] != 0]
+        if bad:
+            lines.append("# passes with a non-zero exit kept for their complete results: "
+                         + ", ".join(bad))
     return "\n".join(lines) + "\n"
 
 
@@ -189,11 +244,12 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
     from paper_2608_21157_amd.inputs import WORKLOADS as WL
 
     os.makedirs(dest, exist_ok=True)
+    statuses = pass_statuses(out)
     fscale, wscale, cf, cw = copy_calibration(out)
     cst = [r for r in kernel_stats(out, "copy") if COPY_KERNEL in r["Name"]][0]
     with open(os.path.join(dest, "copy_probe_1GiB_calibration.txt"), "w") as f:
         f.write("# Copy probe, 1 GiB read + 1 GiB written per dispatch (counter calibration)\n")
-        f.write(fmt_cmds("copy"))
+        f.write(fmt_cmds("copy", statuses))
         f.write("kernel                      %s\n" % COPY_KERNEL)
         f.write("calls                       %s\n" % cst["Calls"])
         f.write("average duration (ns)       %.0f\n" % float(cst["AverageNs"]))
@@ -228,7 +284,7 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
         fname = "%s_%s_%s_%s.txt" % (KERNELS[kern], w, "x".join(map(str, wl.dims)), wl.dtype)
         with open(os.path.join(dest, fname), "w") as f:
             f.write("# %s on %s\n" % (kern, bench.describe(wl)))
-            f.write(fmt_cmds(w))
+            f.write(fmt_cmds(w, statuses))
             f.write("# kernel source sha256[:16] of the profiled build: %s\n" % sha)
             f.write("kernel stats (--kernel-trace --stats):\n")
             for r in stats:

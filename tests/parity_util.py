@@ -1,11 +1,15 @@
-"""Shared helpers of the GPU parity tests: run the library through the C ABI, pick sample
-points, and state the tolerance.
+"""Shared helpers of the GPU parity tests: run the library through the C ABI, compare
+with the oracle (whole grids, or full-size grids piece by piece), and state the
+tolerance.
 
 Tolerance (fp32): max |gpu - oracle| <= 1e-5 * max(steps, 1) * max(1, max|x|) * max(1, max k).
 The 1e-5-per-step bar assumes inputs in [-1, 1] and sum|w| <= 1; inputs of larger magnitude
 (the N(0,1) conv-form workload) scale it by max|x|.  The worst-case fp32 rounding of a
 27-term sum is 27 * 2^-24 * sum|w| * max|x| ~ 1.6e-6 * max|x|, below the bar.
-Tolerance (fp64): 1e-12 * max(steps, 1) * max(1, max|x|).
+Tolerance (fp64): a flat 1e-12, whatever the step count or the input's magnitude.  The
+worst-case fp64 rounding of the largest case here (27 terms, N(0,1) input with max|x| ~ 5.4)
+is 27 * 2^-53 * 5.4 ~ 1.6e-14 per step, and every multi-step workload is non-expansive
+(sum|w| <= 1), so the flat bar holds with two orders of magnitude to spare.
 """
 from __future__ import annotations
 
@@ -16,18 +20,24 @@ import oracle
 from paper_2608_21157_amd import binding as B
 
 
+FP32_PER_STEP = 1e-5
+FP64_FLAT = 1e-12
+
+
 def tolerance(wl, x, k=None, steps=None) -> float:
+    if wl.dtype != "f32":
+        return FP64_FLAT
     steps = wl.steps if steps is None else steps
     scale = max(1.0, float(np.abs(x).max()) if x.size else 1.0)
     if k is not None:
         scale *= max(1.0, float(np.abs(k).max()))
-    base = 1e-5 if wl.dtype == "f32" else 1e-12
-    return base * max(steps, 1) * scale
+    return FP32_PER_STEP * max(steps, 1) * scale
 
 
 def run_library(wl, x, w, k=None, *, steps=None, variant=B.VARIANT_AUTO, depth=0,
-                stream=None, tile=0, grid_scale=0):
-    """Upload, apply through the C ABI, download.  Returns (result float64, plan info)."""
+                stream=None, tile=0, grid_scale=0, as_f64=True):
+    """Upload, apply through the C ABI, download.  Returns (result, plan info); the
+    result is float64, or the computed dtype with ``as_f64=False`` (full-size grids)."""
     steps = wl.steps if steps is None else steps
     dev = torch.device("cuda:0")
     xt = torch.from_numpy(np.ascontiguousarray(x)).to(dev)
@@ -50,7 +60,8 @@ def run_library(wl, x, w, k=None, *, steps=None, variant=B.VARIANT_AUTO, depth=0
         torch.cuda.synchronize()
     finally:
         plan.close()
-    return yt.cpu().numpy().astype(np.float64), info
+    got = yt.cpu().numpy()
+    return (got.astype(np.float64) if as_f64 else got), info
 
 
 def oracle_full(wl, x, w, k=None, steps=None):
@@ -59,39 +70,23 @@ def oracle_full(wl, x, w, k=None, steps=None):
                         steps=steps, field=k, ndim=wl.ndim, channels=wl.channels)
 
 
-def sample_points(wl, x, count: int, seed: int = 0, steps=None):
-    """Sample (b, z, y, x) rows: all corners, points within R*steps of each face, and
-    uniformly random interior points."""
+def dense_report(name, wl, x, w, k, got, tol, steps=None):
+    """``got`` against the oracle at every point of a full-size grid: the oracle runs in
+    independent slabs or volumes on host threads (``oracle/whole_grid.py``)."""
+    from oracle import whole_grid
     steps = wl.steps if steps is None else steps
-    g = np.random.default_rng(seed)
-    dims = (1,) + tuple(wl.dims) if wl.ndim == 2 else tuple(wl.dims)
-    lead = x.shape[: x.ndim - wl.ndim]
-    batch = int(np.prod(lead)) if len(lead) else 1
-    reach = wl.radius * max(steps, 1) + 1
-    pts = []
-    for b in sorted({0, batch - 1}):
-        for cz in sorted({0, dims[0] - 1}):
-            for cy in (0, dims[1] - 1):
-                for cx in (0, dims[2] - 1):
-                    pts.append((b, cz, cy, cx))
-    for _ in range(count // 2):   # near a face along one random axis
-        p = [int(g.integers(0, batch))] + [int(g.integers(0, n)) for n in dims]
-        a = int(g.integers(1 if wl.ndim == 3 else 2, 4))
-        d = int(g.integers(0, min(reach, dims[a - 1])))
-        p[a] = d if g.random() < 0.5 else dims[a - 1] - 1 - d
-        pts.append(tuple(p))
-    for _ in range(count - count // 2):
-        pts.append((int(g.integers(0, batch)),) + tuple(int(g.integers(0, n)) for n in dims))
-    return np.array(pts, dtype=np.int64)
-
-
-def gather(result, pts, wl):
-    """Values of a (batch?, *dims) result at (b, z, y, x) rows."""
-    dims = tuple(wl.dims)
-    flat = result.reshape((-1,) + dims)
-    if wl.ndim == 2:
-        return flat[pts[:, 0], pts[:, 2], pts[:, 3]]
-    return flat[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]
+    rep = whole_grid.compare(got, x, w, shape=wl.shape, radius=wl.radius,
+                             boundary=wl.boundary, steps=steps, ndim=wl.ndim,
+                             channels=wl.channels, field=k)
+    print("[parity] %s every point: %d points, max_abs_err=%.3e at flat %d, tol=%.1e, "
+          "nonfinite=%d (oracle %.1f s on %d threads, %d pieces)" % (
+              name, rep["points"], rep["max_abs_err"], rep["worst"], tol, rep["nonfinite"],
+              rep["seconds"], rep["threads"], rep["pieces"]), flush=True)
+    assert rep["points"] == x.size
+    assert rep["nonfinite"] == 0, "%s: non-finite values" % name
+    assert rep["max_abs_err"] <= tol, "%s: max abs error %.3e > %.1e" % (
+        name, rep["max_abs_err"], tol)
+    return rep
 
 
 def report(name, got, ref, tol):

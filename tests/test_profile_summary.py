@@ -42,6 +42,10 @@ def test_summaries_calibrate_counters_and_record_traffic(tmp_path):
     # c2: the fused star kernel, 2 steps per launch over 256^3 fp32 points
     n = 256 ** 3
     _fake_run(out, "stencil_star_tb2_kernel", "c2", 26000, n * 4 / 1024 / 2 / 2, n * 4 / 1024)
+    # one pass ended with a non-zero status after writing its results
+    for name, _, _, _ in profile.passes("c2") + profile.passes("copy"):
+        profile.record_status(out, name, {"status": 139 if name == "pmc_SQ_c2" else 0,
+                                          "seconds": 3.0, "complete": True})
     rec = profile.write_summaries(out, ["c2"], dest=dest)["stencil_star_tb2_kernel/c2"]
     assert rec["fetch_scale"] == 2.0 and rec["write_scale"] == 1.0
     assert rec["algorithmic_bytes_per_launch"] == 8 * n * 2
@@ -51,8 +55,10 @@ def test_summaries_calibrate_counters_and_record_traffic(tmp_path):
     with open(os.path.join(dest, "counters.json")) as f:
         assert json.load(f) == {"stencil_star_tb2_kernel/c2": rec}
     text = open(os.path.join(dest, "star_tb2_c2_256x256x256_f32.txt")).read()
-    assert "rocprofv3 --pmc FETCH_SIZE" in text and "--no-tune --workload c2" in text
+    assert "rocprofv3 --pmc FETCH_SIZE" in text and "--workload c2" in text
     assert "0.375 x algorithmic" in text
+    assert "pmc_FETCH_SIZE_c2 0 (3 s)" in text and "pmc_SQ_c2 139 (3 s)" in text
+    assert "non-zero exit kept for their complete results: pmc_SQ_c2" in text
     assert os.path.exists(os.path.join(dest, "copy_probe_1GiB_calibration.txt"))
 
 
