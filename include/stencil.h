@@ -211,6 +211,38 @@ stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
                             int32_t steps, double tolerance, int32_t reps, hipStream_t stream,
                             stencil_tune_report *report);
 
+/* Sizes of the device scratch stencil_apply_noalloc() uses: one static array per GPU,
+ * held until the process ends. */
+#define STENCIL_NOALLOC_WEIGHT_BYTES (64 * 1024)        /* channels * npoints weights */
+#define STENCIL_NOALLOC_GRID_BYTES (64 * 1024 * 1024)   /* intermediate grid of a call */
+
+/*
+ * stencil_apply_noalloc -- stencil_apply for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, and harnesses that forbid hipMalloc.
+ * It calls no hipMalloc, hipFree or other allocating routine, and it does not use or
+ * create the plan's device buffers.  It runs the same kernels in the same launch
+ * configuration as stencil_apply, so its results are identical.
+ *   Arguments, ownership and checks: those of stencil_apply().
+ *   Scratch: the weights and, for a call of more than one launch, the intermediate grid
+ *     live in a static device array of STENCIL_NOALLOC_WEIGHT_BYTES +
+ *     STENCIL_NOALLOC_GRID_BYTES bytes per GPU, created with the library's code object
+ *     and looked up on the first call on each device.  Nothing in it needs clearing: each
+ *     call uploads its weights (with hipMemcpyAsync on `stream`, staged before the call
+ *     returns) before its first launch.
+ *   Limits: channels * npoints * sizeof(dtype) <= STENCIL_NOALLOC_WEIGHT_BYTES, and, when
+ *     the call makes more than one launch (steps beyond the plan's temporal depth, or
+ *     more than one step on the generic kernel), batch * volume * sizeof(dtype) <=
+ *     STENCIL_NOALLOC_GRID_BYTES; otherwise STENCIL_ERR_UNSUPPORTED, before any HIP call.
+ *   Concurrency: every call on a GPU shares that GPU's scratch.  Calls ordered on one
+ *     stream are safe; calls that overlap in time on one GPU (other streams, other
+ *     threads) race on it and must not be issued.
+ * Returns STENCIL_OK, INVALID_ARG, MISMATCH, ALIAS, UNSUPPORTED or ERR_HIP.
+ */
+stencil_status stencil_apply_noalloc(stencil_plan_t plan, const void *in, void *out,
+                                     const int64_t dims[3], const void *coeffs,
+                                     const void *coeff_field, int32_t radius, int32_t boundary,
+                                     int32_t steps, hipStream_t stream);
+
 /*
  * stencil_destroy -- free a plan and its device memory.  NULL is accepted.  The caller
  * must make sure no enqueued work still uses the plan (synchronise its stream first).

@@ -25,7 +25,10 @@ VARIANT_AUTO, VARIANT_GENERIC, VARIANT_STREAM = 0, 1, 2
 VARIANT_NAMES = {VARIANT_GENERIC: "generic", VARIANT_STREAM: "stream"}
 
 EXPORTED = ("stencil_plan", "stencil_apply", "stencil_destroy", "stencil_plan_query",
-            "stencil_num_points", "stencil_status_str", "stencil_last_error", "stencil_tune")
+            "stencil_num_points", "stencil_status_str", "stencil_last_error", "stencil_tune",
+            "stencil_apply_noalloc")
+NOALLOC_WEIGHT_BYTES = 64 * 1024       # STENCIL_NOALLOC_WEIGHT_BYTES
+NOALLOC_GRID_BYTES = 64 * 1024 * 1024  # STENCIL_NOALLOC_GRID_BYTES
 TUNE_MAX_CANDIDATES = 20
 
 
@@ -83,6 +86,8 @@ def load():
     lib.stencil_apply.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_int64), vp, vp,
                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp]
     lib.stencil_apply.restype = ctypes.c_int
+    lib.stencil_apply_noalloc.argtypes = lib.stencil_apply.argtypes
+    lib.stencil_apply_noalloc.restype = ctypes.c_int
     lib.stencil_destroy.argtypes = [vp]
     lib.stencil_destroy.restype = ctypes.c_int
     lib.stencil_plan_query.argtypes = [vp, ctypes.POINTER(StencilPlanInfo)]
@@ -127,6 +132,17 @@ def stencil_apply(plan: int, inp: int, out: int, dims, coeffs, coeff_field: int 
     cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
     _check(load().stencil_apply(plan, inp, out, d, cp, coeff_field, radius, boundary, steps,
                                 stream))
+
+
+def stencil_apply_noalloc(plan: int, inp: int, out: int, dims, coeffs,
+                          coeff_field: int | None, radius: int, boundary: int, steps: int,
+                          stream: int | None) -> None:
+    """``stencil_apply`` through the library's static scratch (no device allocation);
+    arguments as ``stencil_apply``."""
+    d = dims if isinstance(dims, ctypes.Array) else _dims3(dims)
+    cp = coeffs.ctypes.data if hasattr(coeffs, "ctypes") else coeffs
+    _check(load().stencil_apply_noalloc(plan, inp, out, d, cp, coeff_field, radius, boundary,
+                                        steps, stream))
 
 
 def _dims3(dims) -> ctypes.Array:

@@ -23,7 +23,8 @@ PROBE_LIB = os.path.join(HERE, "libstencil_probe.so")
 ARCH = "gfx950"
 
 SOURCES = ["abi.cpp", "kernel_generic.hip", "kernel_stream.hip", "kernel_box.hip", "kernel_star.hip",
-           "kernel_star_tb.hip", "kernel_star_tbs.hip", "kernel_box2.hip", "kernel_check.hip"]
+           "kernel_star_tb.hip", "kernel_star_tbs.hip", "kernel_box2.hip", "kernel_check.hip",
+           "noalloc.hip"]
 
 # Packed FP32 instructions are kept out of every kernel (-packed-fp32-ops).
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Wno-unused-parameter",

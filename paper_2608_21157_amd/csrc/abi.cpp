@@ -11,14 +11,17 @@
 #include <new>
 #include <string>
 
+#include "entry.hpp"
 #include "plan.hpp"
 
 using stencil::Geometry;
 using stencil::Plan;
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace stencil {
 
 stencil_status fail(stencil_status st, const char *fmt, ...)
 {
@@ -35,6 +38,18 @@ stencil_status hip_fail(hipError_t e, const char *what)
 {
     return fail(STENCIL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+void clear_error()
+{
+    g_last_error.clear();
+}
+
+}  // namespace stencil
+
+using stencil::fail;
+using stencil::hip_fail;
+
+namespace {
 
 int32_t points(int32_t shape, int32_t ndim, int32_t radius)
 {
@@ -128,7 +143,11 @@ bool aligned16(const void *p)
     return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
 }
 
-// Host-side checks shared by stencil_apply and stencil_tune.
+}  // namespace
+
+namespace stencil {
+
+// Host-side checks shared by the apply entry points and stencil_tune.
 stencil_status check_call(const Plan *p, const void *in, const void *out, const int64_t dims[3],
                           const void *coeffs, const void *coeff_field, int32_t radius,
                           int32_t boundary, int32_t steps)
@@ -160,6 +179,58 @@ stencil_status check_call(const Plan *p, const void *in, const void *out, const 
         return fail(STENCIL_ERR_ALIAS, "out overlaps the coefficient field");
     return STENCIL_OK;
 }
+
+bool runs_fast(const Plan *p, const void *in, const void *out, const void *coeff_field)
+{
+    // fast kernels use 16-byte vector accesses; misaligned pointers run the generic kernel
+    return p->variant == STENCIL_VARIANT_STREAM && aligned16(in) && aligned16(out) &&
+           (coeff_field == nullptr || aligned16(coeff_field));
+}
+
+int launch_count(const Plan *p, bool fast, int steps)
+{
+    const int depth = fast ? p->depth : 1;
+    return (steps + depth - 1) / depth;
+}
+
+stencil_status enqueue_steps(const Plan *p, bool fast, const void *in, void *out,
+                             const void *coeff_field, const void *w, void *grid, int steps,
+                             hipStream_t stream)
+{
+    const Geometry &g = p->geo;
+    hipError_t e;
+    if (steps == 0) {
+        const size_t bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
+        if ((e = hipMemcpyAsync(out, in, bytes, hipMemcpyDeviceToDevice, stream)) != hipSuccess)
+            return hip_fail(e, "hipMemcpyAsync(copy for steps = 0)");
+        return STENCIL_OK;
+    }
+    const int depth = fast ? p->depth : 1;
+    const int launches = launch_count(p, fast, steps);
+    // launch i writes `out` when an even number of launches follows it, so the last one
+    // always lands in `out`; launch i > 0 reads what launch i - 1 wrote
+    const void *src = in;
+    int left = steps;
+    for (int i = 0; i < launches; ++i) {
+        const int d = left < depth ? left : depth;
+        void *dst = ((launches - 1 - i) % 2 == 0) ? out : grid;
+        if (fast)
+            e = launch_stream(g, src, dst, coeff_field, w, d, stream);
+        else
+            e = launch_generic(g, src, dst, coeff_field, w, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "kernel launch");
+        src = dst;
+        left -= d;
+    }
+    return STENCIL_OK;
+}
+
+}  // namespace stencil
+
+using stencil::check_call;
+
+namespace {
 
 // A launch configuration: what stencil_tune varies and fixes in the plan.
 struct Config {
@@ -314,13 +385,8 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
         check_call(p, in, out, dims, coeffs, coeff_field, radius, boundary, steps);
     if (st != STENCIL_OK)
         return st;
-    const size_t bytes = size_t(g.batch) * size_t(g.vol) * g.elt;
-
-    // fast kernels use 16-byte vector accesses; misaligned pointers run the generic kernel
-    const bool fast = p->variant == STENCIL_VARIANT_STREAM && aligned16(in) && aligned16(out) &&
-                      (coeff_field == nullptr || aligned16(coeff_field));
-    const int depth = fast ? p->depth : 1;
-    const int launches = (steps + depth - 1) / depth;
+    const bool fast = stencil::runs_fast(p, in, out, coeff_field);
+    const int launches = stencil::launch_count(p, fast, steps);
 
     // ---- device state (first use) --------------------------------------------------
     int dev = -1;
@@ -379,28 +445,8 @@ stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,
     }
 
     // ---- steps ------------------------------------------------------------------------
-    if (steps == 0) {
-        if ((e = hipMemcpyAsync(out, in, bytes, hipMemcpyDeviceToDevice, stream)) != hipSuccess)
-            return hip_fail(e, "hipMemcpyAsync(copy for steps = 0)");
-        return STENCIL_OK;
-    }
-    // launch i writes `out` when an even number of launches follows it, so the last one
-    // always lands in `out`; launch i > 0 reads what launch i - 1 wrote
-    const void *src = in;
-    int left = steps;
-    for (int i = 0; i < launches; ++i) {
-        const int d = left < depth ? left : depth;
-        void *dst = ((launches - 1 - i) % 2 == 0) ? out : p->scratch;
-        if (fast)
-            e = stencil::launch_stream(g, src, dst, coeff_field, p->d_coeff, d, stream);
-        else
-            e = stencil::launch_generic(g, src, dst, coeff_field, p->d_coeff, stream);
-        if (e != hipSuccess)
-            return hip_fail(e, "kernel launch");
-        src = dst;
-        left -= d;
-    }
-    return STENCIL_OK;
+    return stencil::enqueue_steps(p, fast, in, out, coeff_field, p->d_coeff, p->scratch, steps,
+                                  stream);
 }
 
 stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,

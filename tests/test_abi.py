@@ -268,3 +268,65 @@ def test_valid_tune_without_gpu_reports_hip_error(plan):
         pytest.skip("a GPU is present")
     assert tune_status(plan, steps=2) == B.ERR_HIP
     assert "hipGetDevice" in B.stencil_last_error()
+
+
+def noalloc_status(h, inp=IN, out=OUT, dims=(4, 5, 6), coeffs=W27, field=FIELD, radius=1,
+                   boundary=B.ZERO, steps=1):
+    return status_of(B.stencil_apply_noalloc, h, inp, out, dims, coeffs, field, radius,
+                     boundary, steps, None)
+
+
+def test_noalloc_validation_matches_apply(plan):
+    """The allocation-free entry point makes stencil_apply's checks, with its statuses."""
+    for kw in (dict(inp=None), dict(coeffs=None), dict(steps=-1), dict(dims=(4, 5, 7)),
+               dict(radius=2), dict(boundary=B.PERIODIC), dict(field=None), dict(out=IN),
+               dict(out=FIELD + 8)):
+        assert noalloc_status(plan, **kw) == apply_status(plan, **kw) != B.OK
+    assert noalloc_status(None) == B.ERR_INVALID_ARG
+
+
+def test_noalloc_scratch_limits_are_checked_before_any_hip_call():
+    """A call that needs an intermediate grid larger than the static scratch, or weights
+    larger than its weight region, is refused on the host, even without a GPU."""
+    limit = B.NOALLOC_GRID_BYTES
+    # 256^3 fp32 is exactly the grid region: its multi-launch calls fit
+    fits = B.stencil_plan(desc3(dims=(256, 256, 256)))
+    big = B.stencil_plan(desc3(dims=(257, 256, 256)))
+    w7 = np.zeros(7, np.float32)
+    try:
+        assert 256 ** 3 * 4 == limit
+        # beyond the Infinity Cache the planner fuses four steps per launch
+        assert B.stencil_plan_query(big).temporal_depth == 4
+        kw = dict(dims=(257, 256, 256), coeffs=w7, field=None, out=OUT + (1 << 30))
+        assert noalloc_status(big, steps=5, **kw) == B.ERR_UNSUPPORTED   # 2 launches
+        assert "intermediate grid" in B.stencil_last_error()
+        import torch
+        if not torch.cuda.is_available():
+            # one launch (four fused steps) and 0 steps need no grid: they reach HIP
+            assert noalloc_status(big, steps=4, **kw) == B.ERR_HIP
+            assert noalloc_status(big, steps=0, **kw) == B.ERR_HIP
+            kw["dims"] = (256, 256, 256)
+            assert noalloc_status(fits, steps=5, **kw) == B.ERR_HIP
+    finally:
+        B.stencil_destroy(fits)
+        B.stencil_destroy(big)
+    # 64 KiB of weights: 304 weight sets of 27 fp64 values do not fit, 303 do
+    for channels, status in ((304, B.ERR_UNSUPPORTED), (303, B.ERR_HIP)):
+        h = B.stencil_plan(desc3(dims=(4, 5, 6), shape=B.BOX, dtype=B.F64, batch=channels,
+                                 channels=channels))
+        try:
+            import torch
+            if status == B.ERR_HIP and torch.cuda.is_available():
+                continue
+            w = np.zeros(channels * 27, np.float64)
+            assert noalloc_status(h, coeffs=w, field=None, out=OUT + (1 << 30)) == status
+        finally:
+            B.stencil_destroy(h)
+    assert 303 * 27 * 8 <= B.NOALLOC_WEIGHT_BYTES < 304 * 27 * 8
+
+
+def test_noalloc_limits_match_the_header():
+    text = open(HEADER).read()
+    assert re.search(r"STENCIL_NOALLOC_WEIGHT_BYTES \(64 \* 1024\)", text)
+    assert re.search(r"STENCIL_NOALLOC_GRID_BYTES \(64 \* 1024 \* 1024\)", text)
+    assert B.NOALLOC_WEIGHT_BYTES == 64 * 1024 and B.NOALLOC_GRID_BYTES == 64 << 20
