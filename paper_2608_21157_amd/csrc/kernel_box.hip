@@ -54,7 +54,7 @@ __device__ __forceinline__ T madd(T a, T b, T c)
     return fma(a, b, c);
 }
 
-template <typename T, int TY, bool PERIODIC, bool FIELD, int STORE_CP, int INNER_CP>
+template <typename T, int TY, bool PERIODIC, bool FIELD, int STORE_CP, int INNER_CP, bool XHALO>
 __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
     const T *__restrict__ in, T *__restrict__ out, const T *__restrict__ field,
     const T *__restrict__ w, BoxParams p)
@@ -103,7 +103,9 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
         W[j] = wb[up ? j : (2 - j / 9) * 9 + j % 9];
 
     // byte offsets of input rows y0 - 1 .. y0 + TY within a plane; rows outside the grid
-    // (zero boundary) get an offset past the resource and read as zero
+    // (zero boundary) get an offset past the resource and read as zero.  Without XHALO
+    // (a segment is a whole row under the zero boundary) the x halo is the zero padding:
+    // no halo loads and no halo registers
     const bool first = lx == 0, last = lx == p.lpr - 1;
     int hx = first ? seg * p.segw - 1 : seg * p.segw + p.segw;
     bool hok = (first || last) && hx >= 0 && hx < p.nx;
@@ -111,7 +113,8 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
         hx = wrap_index(hx, p.nx);
         hok = first || last;
     }
-    int ro[NR], ho[NR];
+    constexpr int NH = XHALO ? NR : 1;
+    int ro[NR], ho[NH];
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
         int yi = y0 - 1 + i;
@@ -121,7 +124,8 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
             ok = true;
         }
         ro[i] = ok ? (yi * p.nx + x) * E : kOutOfRange;
-        ho[i] = (ok && hok) ? (yi * p.nx + hx) * E : kOutOfRange;
+        if (XHALO)
+            ho[i] = (ok && hok) ? (yi * p.nx + hx) * E : kOutOfRange;
     }
 
     // resource of input plane z_in; under the zero boundary a plane outside the grid
@@ -145,14 +149,15 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
                 acc[s][o][e] = T(0);
 
     Vec16<T> rows[NR];
-    T halo[NR];
+    T halo[NH];
     Vec16<T> kv[TY];
     {
         const auto r0 = plane_rsrc(zin(0));
 #pragma unroll
         for (int i = 0; i < NR; ++i) {
             rows[i] = bload16<T>(r0, ro[i]);
-            halo[i] = bload1(r0, ho[i], T(0));
+            if (XHALO)
+                halo[i] = bload1(r0, ho[i], T(0));
         }
     }
     auto load_field = [&](int q) {
@@ -180,10 +185,17 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
 #pragma unroll
         for (int i = 0; i < NR; ++i) {
             T r[VEC + 2];
-            const T left = from_left_lane(rows[i].e[VEC - 1], halo[i]);
-            const T right = from_right_lane(rows[i].e[0], halo[i]);
-            r[0] = first ? halo[i] : left;
-            r[VEC + 1] = last ? halo[i] : right;
+            if constexpr (XHALO) {
+                const T left = from_left_lane(rows[i].e[VEC - 1], halo[i]);
+                const T right = from_right_lane(rows[i].e[0], halo[i]);
+                r[0] = first ? halo[i] : left;
+                r[VEC + 1] = last ? halo[i] : right;
+            } else {
+                const T left = from_left_lane_or_zero(rows[i].e[VEC - 1]);
+                const T right = from_right_lane_or_zero(rows[i].e[0]);
+                r[0] = first ? T(0) : left;
+                r[VEC + 1] = last ? T(0) : right;
+            }
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
                 r[e + 1] = rows[i].e[e];
@@ -193,7 +205,8 @@ __global__ __launch_bounds__(256) void stencil_box3_stream_kernel(
             // halo) and may be streamed past the caches (INNER_CP)
             rows[i] = (i >= 2 && i <= TY - 1) ? bload16<T, INNER_CP>(rn, more ? ro[i] : kOutOfRange)
                                               : bload16<T>(rn, more ? ro[i] : kOutOfRange);
-            halo[i] = bload1(rn, more ? ho[i] : kOutOfRange, T(0));
+            if (XHALO)
+                halo[i] = bload1(rn, more ? ho[i] : kOutOfRange, T(0));
 #pragma unroll
             for (int a = 0; a < 3; ++a) {
                 if (FIELD ? (k - a < 0 || k - a >= n) : (decltype(check)::value && k - a < 0))
@@ -317,14 +330,20 @@ hipError_t launch_icp(const BoxParams &p, const Geometry &g, const void *src, vo
     const T *wt = static_cast<const T *>(w);
     const dim3 grid(p.nblocks), block(256);
     const bool per = g.boundary == STENCIL_PERIODIC;
+    // a whole row per segment under the zero boundary: the x halo is the padding
+    const bool xhalo = per || p.segs > 1;
     if (per && g.field)
-        stencil_box3_stream_kernel<T, TY, true, true, CP, ICP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, true, true, CP, ICP, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else if (per)
-        stencil_box3_stream_kernel<T, TY, true, false, CP, ICP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, true, false, CP, ICP, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    else if (g.field && xhalo)
+        stencil_box3_stream_kernel<T, TY, false, true, CP, ICP, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else if (g.field)
-        stencil_box3_stream_kernel<T, TY, false, true, CP, ICP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, false, true, CP, ICP, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+    else if (xhalo)
+        stencil_box3_stream_kernel<T, TY, false, false, CP, ICP, true><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     else
-        stencil_box3_stream_kernel<T, TY, false, false, CP, ICP><<<grid, block, 0, stream>>>(s, d, k, wt, p);
+        stencil_box3_stream_kernel<T, TY, false, false, CP, ICP, false><<<grid, block, 0, stream>>>(s, d, k, wt, p);
     return hipGetLastError();
 }
 
