@@ -302,13 +302,15 @@ BoxParams make_params(const Geometry &g)
     p.ygroups = (p.ywaves + 3) / 4;
     p.channels = g.channels;
     const long long base = g.batch * p.segs * p.ygroups;
-    // up to 8192 workgroups (32 per CU), in chunks of at least 16 planes; grid_scale
+    // up to 16384 workgroups (64 per CU), in chunks of at least 8 planes; grid_scale
     // scales the workgroup target and, when positive, shortens the minimum chunk to
-    // 16 >> grid_scale planes.  Measured against the former 2048-workgroup target with
-    // 8-plane chunks: c5 (256 volumes of 128^3) 664 -> 696 Gpoints/s, c4 and c5b level.
-    const long long target = scaled_target(8192, g.grid_scale);
+    // 8 >> grid_scale planes (at least 4).  Same-box A/B against 8192 workgroups of at
+    // least 16 planes: 256 volumes of 128^3 fp32 0.7566 -> 0.7379 and 0.7605 -> 0.7403 ms
+    // (8192 instead of 4096 workgroups), 64 volumes of 128^3 fp64 0.3601 -> 0.3573 ms,
+    // 512^3 with a field level.
+    const long long target = scaled_target(16384, g.grid_scale);
     long long nzc = (target + base - 1) / base;
-    const long long min_len = g.grid_scale > 0 ? std::max(4, 16 >> g.grid_scale) : 16;
+    const long long min_len = g.grid_scale > 0 ? std::max(4, 8 >> g.grid_scale) : 8;
     const long long max_chunks = (p.nz + min_len - 1) / min_len;
     if (nzc > max_chunks)
         nzc = max_chunks;
