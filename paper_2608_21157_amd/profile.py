@@ -186,6 +186,23 @@ def counters(out: str, workload: str, group: str, kernel: str) -> dict:
     return {k: (sum(v) / len(v), len(v)) for k, v in vals.items()}
 
 
+def steady_durations(out: str, workload: str, kernel: str, last: int = 100):
+    """(median, mean of the last `last` launches) of a kernel's durations in ns from the
+    trace pass, or None: the summary's plain average also counts the first calls, which
+    run slower while the GPU warms up."""
+    path = os.path.join(out, "trace_" + workload, workload + "_kernel_trace.csv")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in csv.DictReader(f)
+             if kernel in r["Kernel_Name"]]
+    if not d:
+        return None
+    d_sorted = sorted(d)
+    tail = d[-last:]
+    return d_sorted[len(d_sorted) // 2], sum(tail) / len(tail), len(tail)
+
+
 def copy_calibration(out: str) -> tuple:
     fetch = counters(out, "copy", "FETCH_SIZE", COPY_KERNEL)["FETCH_SIZE"][0]
     write = counters(out, "copy", "WRITE_SIZE", COPY_KERNEL)["WRITE_SIZE"][0]
@@ -280,6 +297,8 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
             "fetch_kib_per_dispatch": round(fetch, 1), "write_kib_per_dispatch": round(write, 1),
             "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
             "hbm_bytes_per_launch": int(hbm), "algorithmic_bytes_per_launch": int(algo),
+            "steady_launch_ns": round(steady_durations(out, w, kern)[1], 1)
+            if steady_durations(out, w, kern) else None,
             "traffic_over_algorithmic": round(hbm / algo, 4)}
         fname = "%s_%s_%s_%s.txt" % (KERNELS[kern], w, "x".join(map(str, wl.dims)), wl.dtype)
         with open(os.path.join(dest, fname), "w") as f:
@@ -290,11 +309,19 @@ def write_summaries(out: str, workloads, dest: str = PROFILES) -> dict:
             for r in stats:
                 f.write("  %-100s calls %4d  avg %12.1f ns  %6.2f %%\n" % (
                     r["Name"][:100], int(r["Calls"]), float(r["AverageNs"]), float(r["Percentage"])))
+            sd = steady_durations(out, w, kern)
+            if sd:
+                f.write("duration median (ns)              %.1f\n" % sd[0])
+                f.write("duration, mean of the last %d     %.1f  (steady state; the average above"
+                        " also counts the warm-up launches)\n" % (sd[2], sd[1]))
             f.write("stencil steps per launch          %d\n" % depth)
             f.write("algorithmic bytes per launch      %d  (%d B per point-step x %d points x %d)\n"
                     % (algo, bytes_pt, wl.points_per_step, depth))
             f.write("achieved (algorithmic / avg)      %.1f GB/s  = %.4f of 8 TB/s\n"
                     % (algo / avg_ns, algo / avg_ns / 8000))
+            if sd:
+                f.write("achieved (algorithmic / steady)   %.1f GB/s  = %.4f of 8 TB/s\n"
+                        % (algo / sd[1], algo / sd[1] / 8000))
             f.write("FETCH_SIZE per dispatch           %.1f KiB  (n=%d) x %.4f (copy calibration)\n"
                     % (fetch, nf, fscale))
             f.write("WRITE_SIZE per dispatch           %.1f KiB  (n=%d) x %.4f\n" % (write, nw, wscale))
