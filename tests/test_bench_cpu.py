@@ -76,3 +76,48 @@ def test_code_hash_ignores_comments_but_not_code():
     other = "int f(int a) { return a + 2; }\n"
     assert bench.code_only(src) == bench.code_only(same)
     assert bench.code_only(src) != bench.code_only(other)
+
+
+def test_tolerance_rule():
+    import numpy as np
+    x = np.full(8, 0.5, np.float32)
+    assert bench.tolerance(WORKLOADS["c3"], x) == pytest.approx(4e-5)          # 1e-5 x 4 steps
+    big = np.array([-6.0, 2.0], np.float32)
+    assert bench.tolerance(WORKLOADS["c5"], big) == pytest.approx(6e-5)        # x max|x|
+    k = np.array([0.5, 2.0], np.float32)
+    assert bench.tolerance(WORKLOADS["c4"], x, k) == pytest.approx(2e-5)       # x max k
+    assert bench.tolerance(WORKLOADS["c5b"], big * 100) == 1e-12               # flat fp64
+    assert bench.tolerance(WORKLOADS["paper"], x) == 1e-12
+
+
+def test_protocol_record_grades_the_median():
+    wl = WORKLOADS["c3"]
+    rec = bench.protocol_record(wl, [0.7, 0.5, 0.6, 0.9])
+    assert rec["median_ms"] == pytest.approx(0.65) and rec["min_ms"] == 0.5
+    assert rec["gpoints_per_s_median"] == bench.figures(wl, 0.65)["gpoints_per_s"]
+    assert rec["calls"] == 4
+
+
+@pytest.mark.parametrize("name,dims", [("c3", (13, 11, 16)), ("c4", (9, 7, 8)),
+                                       ("c5b", (5, 6, 8)), ("paper", (20, 17))])
+def test_oracle_check_passes_the_oracle_and_fails_a_planted_error(name, dims):
+    """The bench's whole-grid check accepts the oracle's own result rounded to the
+    workload's dtype, and flags one perturbed point (and a NaN)."""
+    import numpy as np
+    import oracle
+    from paper_2608_21157_amd import inputs
+    wl = WORKLOADS[name].resized(dims, n=1 if WORKLOADS[name].batch > 1 else None,
+                                 steps=min(WORKLOADS[name].steps, 3))
+    x, w, k = inputs.make(wl)
+    ref = oracle.apply(x, w, shape=wl.shape, radius=wl.radius, boundary=wl.boundary,
+                       steps=wl.steps, field=k, ndim=wl.ndim, channels=wl.channels)
+    got = ref.astype(x.dtype)
+    rec = bench.oracle_check(wl, x, w, k, got, "test")
+    assert rec["pass"] and rec["points"] == x.size and rec["nonfinite"] == 0
+    bad = got.copy()
+    bad.flat[x.size // 2] += 10 * rec["tolerance"]
+    rec = bench.oracle_check(wl, x, w, k, bad, "test")
+    assert not rec["pass"] and rec["worst_flat_index"] == x.size // 2
+    bad.flat[0] = np.nan
+    rec = bench.oracle_check(wl, x, w, k, bad, "test")
+    assert not rec["pass"] and rec["nonfinite"] == 1
