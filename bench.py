@@ -377,12 +377,19 @@ PATTERN_PROBES = {"c4": ("triad", 1 << 29), "c5": ("copy", 1 << 31), "c5b": ("co
 def tune_context(torch, B, head, K: int, W: int, reps: int = 10) -> dict:
     """stencil_tune on a runner's workload (a fresh plan of the same description, the same
     buffers; `reps` timed calls per candidate), then K calls of the tuned plan timed like
-    the default plan.  Context only: every reported value is the planner's default plan."""
+    the default plan: a 0.3 s spin-up on its own calls and W warm-up calls first.  Context
+    only: every reported value is the planner's default plan."""
     plan = B.Plan(head.plan.desc)
     try:
         rep = plan.tune(head.x, head.y, head.w, steps=head.wl.steps, field=head.k, reps=reps,
                         stream=head.stream)
         info = plan.info()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.3:
+            for _ in range(5):
+                plan.run(head.x, head.y, head.w, steps=head.wl.steps, field=head.k,
+                         stream=head.stream)
+            head.stream.synchronize()
         for _ in range(W):
             plan.run(head.x, head.y, head.w, steps=head.wl.steps, field=head.k,
                      stream=head.stream)
