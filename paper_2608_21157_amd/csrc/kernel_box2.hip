@@ -297,13 +297,13 @@ stencil_box2_tb2_kernel(
     for (int k = 0; k < HXV; ++k)
         halo_off[k] = hok[k] ? hx[k] * E : kOutOfRange;
     const unsigned row_bytes = unsigned(p.nx * E);
+    // a row outside the grid keeps its address (never dereferenced: zero records), which
+    // leaves the address affine in the row index, without a select
     auto row_rsrc = [&](int y, bool live) {
-        bool ok = live && y >= 0 && y < p.ny;
-        if (PERIODIC) {
-            y = wrap_index(y, p.ny);
-            ok = live;
-        }
-        return make_rsrc(src + (long long)(ok ? y : 0) * p.nx, ok ? row_bytes : 0u);
+        if (PERIODIC)
+            return make_rsrc(src + (long long)wrap_index(y, p.ny) * p.nx, live ? row_bytes : 0u);
+        const bool ok = live && unsigned(y) < unsigned(p.ny);  // 0 <= y < ny
+        return make_rsrc(src + (long long)y * p.nx, ok ? row_bytes : 0u);
     };
 
     // input rows y0 - 2R .. y0 + yc - 1 + 2R; u1 rows y0 - R .. y0 + yc - 1 + R
@@ -447,7 +447,7 @@ stencil_box2_tb2_kernel(
             }
             const bool live = r2 >= 0 && r2 < n;
             bstore16<T, STORE_CP>(
-                make_rsrc(dst + (long long)(live ? y0 + r2 : 0) * p.nx, live ? row_bytes : 0u),
+                make_rsrc(dst + (long long)(y0 + r2) * p.nx, live ? row_bytes : 0u),
                 out_off, v);
         }
     };

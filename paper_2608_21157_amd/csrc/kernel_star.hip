@@ -173,12 +173,12 @@ __global__ __launch_bounds__(64 * NW) void stencil_star_stream_kernel(
     const int zs = dir > 0 ? z0 : z0 + n - 1;
 
     auto plane_rsrc = [&](int z) {
-        bool ok = z >= 0 && z < p.nz;
-        if (PERIODIC) {
-            z = wrap_index(z, p.nz);
-            ok = true;
-        }
-        return make_rsrc(src + (ok ? z : 0) * plane, ok ? plane_bytes : 0u);
+        if (PERIODIC)
+            return make_rsrc(src + wrap_index(z, p.nz) * plane, plane_bytes);
+        // a plane outside the grid keeps its address (never dereferenced: zero records),
+        // which leaves the address affine in the iteration, without a select
+        const bool ok = unsigned(z) < unsigned(p.nz);  // 0 <= z < nz
+        return make_rsrc(src + (long long)z * plane, ok ? plane_bytes : 0u);
     };
 
     Vec16<T> Q[NQ][TY];

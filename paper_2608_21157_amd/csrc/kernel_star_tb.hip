@@ -203,14 +203,14 @@ __global__ __launch_bounds__((Tb2Shape<T, R, PF>::THREADS)) void stencil_star_tb
     // loads return 0); periodic planes wrap.  Planes past the chunk's end are loaded
     // harmlessly by the last iterations' prefetches.
     auto plane_rsrc = [&](int z) {
-        bool ok = z >= 0 && z < p.nz;
-        if (PERIODIC) {
-            z = wrap_index(z, p.nz);
-            ok = true;
-        }
-        return make_rsrc(src + (ok ? z : 0) * plane, ok ? plane_bytes : 0u);
+        if (PERIODIC)
+            return make_rsrc(src + wrap_index(z, p.nz) * plane, plane_bytes);
+        // a plane outside the grid keeps its address (never dereferenced: zero records),
+        // which leaves the address affine in the iteration, without a select
+        const bool ok = unsigned(z) < unsigned(p.nz);  // 0 <= z < nz
+        return make_rsrc(src + (long long)z * plane, ok ? plane_bytes : 0u);
     };
-    auto z_inside = [&](int z) { return PERIODIC || (z >= 0 && z < p.nz); };
+    auto z_inside = [&](int z) { return PERIODIC || unsigned(z) < unsigned(p.nz); };
 
     // ---- queues: position i of iteration m (phase m mod NQ) is slot (phase + i) mod NQ
     // q0 position i holds u0 at plane z1 + dir * (i - R), i = 0 .. 2R + PF (the last PF
@@ -357,8 +357,9 @@ __global__ __launch_bounds__((Tb2Shape<T, R, PF>::THREADS)) void stencil_star_tb
         }
         // the resource depends on the uniform iteration only (a per-lane base would make
         // the compiler serialise the store over lanes); the offset masks the lanes
-        const bool full = m >= 2 * R;
-        bstore16<T, STORE_CP>(make_rsrc(dst + (long long)(full ? z2 : 0) * plane, plane_bytes),
+        // before stage 2 has a full queue every lane's offset is out of range, so the
+        // address of plane z2 (then possibly outside the grid) is never dereferenced
+        bstore16<T, STORE_CP>(make_rsrc(dst + (long long)z2 * plane, plane_bytes),
                               st2 ? soff : kOutOfRange, u2);
         // queue position 0 is free: prefetch u0 at plane z1 + dir * (R + PF + 1), first
         // used PF + 1 iterations from now

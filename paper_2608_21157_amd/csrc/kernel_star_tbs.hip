@@ -156,14 +156,14 @@ __global__ __launch_bounds__((TbsShape<T, R, S>::THREADS)) void stencil_star_tbs
     const int iters = n + 2 * B;
 
     auto plane_rsrc = [&](int z) {
-        bool ok = z >= 0 && z < p.nz;
-        if (PERIODIC) {
-            z = wrap_index(z, p.nz);
-            ok = true;
-        }
-        return make_rsrc(src + (ok ? z : 0) * plane, ok ? plane_bytes : 0u);
+        if (PERIODIC)
+            return make_rsrc(src + wrap_index(z, p.nz) * plane, plane_bytes);
+        // a plane outside the grid keeps its address (never dereferenced: zero records),
+        // which leaves the address affine in the iteration, without a select
+        const bool ok = unsigned(z) < unsigned(p.nz);  // 0 <= z < nz
+        return make_rsrc(src + (long long)z * plane, ok ? plane_bytes : 0u);
     };
-    auto z_inside = [&](int z) { return PERIODIC || (z >= 0 && z < p.nz); };
+    auto z_inside = [&](int z) { return PERIODIC || unsigned(z) < unsigned(p.nz); };
 
     // ---- queues: position i of iteration m (phase m mod NQ) is slot (phase + i) mod NQ.
     // q[0] position i: u_0 at z1 + dir (i - R), i = 0 .. 2R + PF (the last PF prefetched);
@@ -268,10 +268,11 @@ __global__ __launch_bounds__((TbsShape<T, R, S>::THREADS)) void stencil_star_tbs
             if (k < S) {
                 q[k][(phase + 2 * R) % NQ] = u;
             } else {
+                // before the last stage has a full queue every lane's offset is out of
+                // range, so plane zk's address (then possibly outside the grid) is unused
                 const bool full = m >= 2 * B;
-                bstore16<T, STORE_CP>(
-                    make_rsrc(dst + (long long)(full ? zk : 0) * plane, plane_bytes),
-                    full ? soff : kOutOfRange, u);
+                bstore16<T, STORE_CP>(make_rsrc(dst + (long long)zk * plane, plane_bytes),
+                                      full ? soff : kOutOfRange, u);
             }
         }
         q[0][phase] = bload16<T>(plane_rsrc(z1 + dir * (R + PF + 1)), qoff);
