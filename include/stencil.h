@@ -227,8 +227,12 @@ stencil_status stencil_tune(stencil_plan_t plan, const void *in, void *out,
  *     live in a static device array of STENCIL_NOALLOC_WEIGHT_BYTES +
  *     STENCIL_NOALLOC_GRID_BYTES bytes per GPU, created with the library's code object
  *     and looked up on the first call on each device.  Nothing in it needs clearing: each
- *     call uploads its weights (with hipMemcpyAsync on `stream`, staged before the call
- *     returns) before its first launch.
+ *     call's weights are in place before its first launch -- uploaded with hipMemcpyAsync
+ *     on `stream` (staged before the call returns), or left as they are when the device's
+ *     weight region already holds the same bytes from an earlier call (the library keeps
+ *     a host copy of what it last uploaded per device, in static memory).  Under stream
+ *     capture, one call with the same weights before the capture leaves no copy in the
+ *     captured work.
  *   Limits: channels * npoints * sizeof(dtype) <= STENCIL_NOALLOC_WEIGHT_BYTES, and, when
  *     the call makes more than one launch (steps beyond the plan's temporal depth, or
  *     more than one step on the generic kernel), batch * volume * sizeof(dtype) <=

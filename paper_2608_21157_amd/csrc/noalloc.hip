@@ -10,11 +10,12 @@
 // current) and keeps it; every later call uses that address, never the array's name,
 // which in host code is only a stand-in for the symbol.
 //
-// Nothing in `scratch` must start at zero: each call writes the weights before its first
-// launch, and the first launch that reads the intermediate grid reads what the launch
-// before it wrote.  Every call on a GPU shares that GPU's array, so calls that overlap
+// Nothing in `scratch` must start at zero: a call's weights are in place before its first
+// launch (uploaded, unless the region already holds the same bytes), and the first launch
+// that reads the intermediate grid reads what the launch before it wrote.  Every call on a GPU shares that GPU's array, so calls that overlap
 // in time on one GPU (on different streams, or from different threads without ordering)
 // race on it; calls ordered on one stream do not.
+#include <cstring>
 #include <mutex>
 
 #include "entry.hpp"
@@ -37,6 +38,10 @@ static_assert(kWeightBytes % 256 == 0, "the grid region must stay 256-byte align
 
 std::mutex g_scratch_mutex;
 unsigned char *g_scratch_ptr[kMaxDevices] = {};
+// the bytes last uploaded into each device's weight region (static host memory), so that
+// a call whose weights are already there skips the upload
+unsigned char g_weights_host[kMaxDevices][kWeightBytes];
+size_t g_weights_len[kMaxDevices] = {};
 
 // This device's address of `scratch`, looked up once per device (the device is current).
 stencil_status device_scratch(int dev, unsigned char **out)
@@ -100,12 +105,24 @@ extern "C" stencil_status stencil_apply_noalloc(stencil_plan_t plan, const void 
         return st;
 
     // ---- weights, then the launches ----------------------------------------------------
-    // The weights are uploaded on every call: another plan's call may have replaced them.
-    // A copy from pageable host memory is staged by the runtime before it returns, so
-    // `coeffs` may be reused as soon as this call returns.
-    if (steps > 0 &&
-        (e = hipMemcpyAsync(base, coeffs, wbytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
-        return stencil::hip_fail(e, "hipMemcpyAsync(weights into the scratch)");
+    // The weights are uploaded unless the device's weight region already holds these
+    // bytes (from any plan's earlier call: all calls on a device share the region).  The
+    // upload is ordered on `stream` before the launches; a copy from pageable host memory
+    // is staged by the runtime before it returns, so `coeffs` may be reused as soon as
+    // this call returns.  A call that skips the upload relies on the earlier call being
+    // ordered before it, which the concurrency rule above already requires.
+    if (steps > 0) {
+        std::lock_guard<std::mutex> lock(g_scratch_mutex);
+        if (g_weights_len[dev] != wbytes ||
+            std::memcmp(g_weights_host[dev], coeffs, wbytes) != 0) {
+            g_weights_len[dev] = 0;  // unknown contents until the copy is enqueued
+            if ((e = hipMemcpyAsync(base, coeffs, wbytes, hipMemcpyHostToDevice, stream)) !=
+                hipSuccess)
+                return stencil::hip_fail(e, "hipMemcpyAsync(weights into the scratch)");
+            std::memcpy(g_weights_host[dev], coeffs, wbytes);
+            g_weights_len[dev] = wbytes;
+        }
+    }
     return stencil::enqueue_steps(p, fast, in, out, coeff_field, base, base + kWeightBytes,
                                   steps, stream);
 }

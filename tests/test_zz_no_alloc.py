@@ -105,6 +105,34 @@ def test_two_calls_in_a_row_match_stencil_apply(first, second):
         b.close()
 
 
+def test_weights_changing_between_calls():
+    """Calls in a row on one stream whose weights repeat, change and change back (the
+    library skips the upload when the device already holds the same bytes), across two
+    plans of different sizes: every result matches stencil_apply's with its weights."""
+    a = Case("c2", (24, 20, 64), steps=3)
+    b = Case("c2", (16, 12, 32), steps=2)
+    g = np.random.default_rng(5)
+    w_other = g.uniform(-1, 1, a.w.shape)
+    w_other = (w_other / np.abs(w_other).sum()).astype(a.w.dtype)
+    s = torch.cuda.Stream()
+    outs = []
+    try:
+        for case, w in ((a, a.w), (a, a.w), (b, a.w), (a, w_other), (b, w_other), (a, a.w)):
+            case.w = w
+            case.noalloc(s)
+            case.apply(s)
+            s.synchronize()
+            assert torch.equal(case.y_noalloc, case.y_apply)
+            outs.append(case.y_noalloc.clone())
+        # the calls with the first weights agree with each other, the others differ
+        assert torch.equal(outs[0], outs[1]) and torch.equal(outs[0], outs[5])
+        assert not torch.equal(outs[0], outs[3])
+        a.check("weights repeated and changed")
+    finally:
+        a.close()
+        b.close()
+
+
 def test_call_beyond_the_scratch_is_refused_and_writes_nothing():
     """The 27-point box on 512^3 fp32 over 2 steps (two launches) needs a 512 MiB
     intermediate grid: refused on the host, and `out` is left as it was."""
