@@ -743,14 +743,20 @@ def main() -> int:
     return 0
 
 
+def timed_calls(s_per_call: float, window_s: float = 0.05) -> int:
+    """Back-to-back calls for a timed window of about `window_s` (20 to 5000): a window of a
+    few calls would be dominated by the first launch's latency on a launch-bound workload."""
+    return int(min(5000, max(20, window_s / max(s_per_call, 1e-9))))
+
+
 def workload_leg(torch, B, inputs, wl, stream, flush, args, checks_todo) -> dict:
-    """One workload of the per-workload block: spin-up on its own kernel, 20 back-to-back
-    calls after 20 warm-up calls, the flushed protocol, the tuner's choice, and (queued
+    """One workload of the per-workload block: spin-up on its own kernel, about 50 ms of
+    back-to-back calls (20 at least) after 20 warm-up calls, the flushed protocol, the tuner's choice, and (queued
     for the CPU phase) its output for the whole-grid oracle check."""
     r = Runner(torch, B, inputs, wl, stream)
     paper = wl.name == "paper"
-    r.spin(0.3)
-    reps = 3 if paper else 20
+    spun = r.spin(0.3)
+    reps = 3 if paper else timed_calls(0.3 / spun)
     t = r.timed(reps, 1 if paper else 20) / reps
     rec = figures(wl, t)
     rec.update(kernel=r.kernel, variant=r.variant, depth=r.depth, tile=r.tile,

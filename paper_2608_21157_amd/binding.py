@@ -3,7 +3,10 @@
 Argument marshalling only: every step of the operator runs in the library's HIP kernels.
 The functions keep the C names (``stencil_plan``, ``stencil_apply``, ``stencil_destroy``,
 ...) and raise ``StencilError`` on a non-OK status.  ``Plan`` and ``apply`` are thin
-conveniences over them for torch tensors (torch supplies device memory and streams).
+conveniences over them for torch tensors (torch supplies device memory and streams);
+``Plan.run`` calls ``stencil_apply`` through the small CPython extension ``_fastcall``
+(built from ``csrc/fastcall.c`` against the same library), which converts ten integers
+per call where ctypes would convert ten objects.
 
 The library must have been built (``python -m paper_2608_21157_amd.build``); there is no
 fallback: loading fails loudly when it is missing.
@@ -68,7 +71,8 @@ class StencilError(RuntimeError):
 
 
 _lib = None
-_raw_apply = None   # stencil_apply without argtypes, for Plan.run's pre-built arguments
+_NO_STREAM = object()   # Plan._sh_obj before the first run: matches no argument, not even None
+_fast_apply = None   # _fastcall.apply: stencil_apply with integer arguments, for Plan.run
 
 
 def load():
@@ -102,11 +106,11 @@ def load():
                                  ctypes.c_int32, ctypes.c_double, ctypes.c_int32, vp,
                                  ctypes.POINTER(StencilTuneReport)]
     lib.stencil_tune.restype = ctypes.c_int
-    global _raw_apply
-    # a second handle of the same library, so that this function object has no argtypes:
-    # Plan.run passes ctypes objects only, and the call then converts nothing
-    _raw_apply = ctypes.CDLL(LIB_PATH).stencil_apply
-    _raw_apply.restype = ctypes.c_int
+    global _fast_apply
+    # linked against libstencil.so by name with an $ORIGIN run path: the loader finds the
+    # library loaded above (same file), so both share one set of plans and error state
+    from . import _fastcall
+    _fast_apply = _fastcall.apply
     _lib = lib
     return lib
 
@@ -216,6 +220,7 @@ class Plan:
         self.handle = stencil_plan(desc)
         self.dims = tuple(desc.dims[i] for i in range(desc.ndim))
         self._dims_c = _dims3(self.dims)  # built once: run() is on the latency path
+        self._dims_addr = ctypes.addressof(self._dims_c)
         self._numel = int(desc.batch)
         for d in self.dims:
             self._numel *= int(d)
@@ -223,15 +228,12 @@ class Plan:
                                                                 desc.radius)
         self._stream = None               # last stream run on (close() waits for it)
         self._seen = (None, None, None, None)   # x, y, field, coeffs last validated
-        self._sh_obj = None               # stream object whose handle is in _sh
-        # pre-built arguments of the raw call (no per-call ctypes conversion)
-        vp = ctypes.c_void_p
-        self._raw = _raw_apply
-        self._h = vp(self.handle)
-        self._pin, self._pout, self._pfield, self._pc, self._sh = vp(), vp(), vp(), vp(), vp()
-        self._radius_c = ctypes.c_int32(desc.radius)
-        self._bnd_c = ctypes.c_int32(desc.boundary)
-        self._steps_c = ctypes.c_int32(0)
+        self._sh_obj = _NO_STREAM         # stream argument whose handle is in _sh
+        self._sh = 0                      # that stream's handle (0: the null stream)
+        self._fast = _fast_apply
+        self._pc = 0                      # address of the weights last validated
+        self._radius = int(desc.radius)
+        self._boundary = int(desc.boundary)
 
     def info(self) -> StencilPlanInfo:
         return stencil_plan_query(self.handle)
@@ -270,30 +272,23 @@ class Plan:
         if any(d.type != "cuda" for d in devs) or len(devs) != 1:
             raise ValueError("x, y (and field) must be CUDA tensors on one device")
         self._seen = (x, y, field, coeffs)
-        self._pc.value = coeffs.ctypes.data
+        self._pc = coeffs.ctypes.data
 
     def run(self, x, y, coeffs, *, steps: int, field=None, stream=None) -> None:
         seen = self._seen
         if x is not seen[0] or y is not seen[1] or field is not seen[2] or coeffs is not seen[3]:
             self._validate(x, y, coeffs, field)
-        if stream is None:
-            import torch
-            stream = torch.cuda.current_stream()
         if stream is not self._sh_obj:
-            self._sh.value = stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+            if stream is None:
+                import torch
+                stream = torch.cuda.current_stream()
+            self._sh = (stream.cuda_stream if hasattr(stream, "cuda_stream") else stream) or 0
             self._sh_obj = stream
         self._stream = stream
-        self._pin.value = x.data_ptr()
-        self._pout.value = y.data_ptr()
-        pf = None
-        if field is not None:
-            self._pfield.value = field.data_ptr()
-            pf = self._pfield
-        if self._steps_c.value != steps:
-            self._steps_c.value = steps
-        st = self._raw(self._h, self._pin, self._pout, self._dims_c, self._pc, pf,
-                       self._radius_c, self._bnd_c, self._steps_c, self._sh)
-        if st != OK:
+        st = self._fast(self.handle or 0, x.data_ptr(), y.data_ptr(), self._dims_addr,
+                        self._pc, 0 if field is None else field.data_ptr(), self._radius,
+                        self._boundary, steps, self._sh)
+        if st:
             _check(st)
 
     def tune(self, x, y, coeffs, *, steps: int, field=None, tolerance: float = -1.0,
@@ -321,13 +316,12 @@ class Plan:
     def close(self) -> None:
         """Wait for the last stream this plan ran on, then free the plan."""
         self._seen = (None, None, None, None)
-        self._sh_obj = None
+        self._sh_obj = _NO_STREAM
         if self.handle:
             if self._stream is not None and hasattr(self._stream, "synchronize"):
                 self._stream.synchronize()
             stencil_destroy(self.handle)
             self.handle = None
-            self._h.value = None
 
     def __del__(self):
         try:

@@ -1,8 +1,9 @@
 """Build the HIP library ``libstencil.so`` for gfx950 with hipcc.
 
-Every source under ``csrc/`` is compiled to an object in ``_build/`` (in parallel) and
-linked into ``libstencil.so`` next to this file.  ``build()`` always recompiles.  A
-kernel that uses scratch memory fails the build.
+Every HIP/C++ source under ``csrc/`` is compiled to an object in ``_build/`` (in parallel)
+and linked into ``libstencil.so`` next to this file; ``csrc/fastcall.c`` becomes the
+binding's CPython extension, linked against it.  ``build()`` always recompiles.  A kernel
+that uses scratch memory fails the build.
 """
 from __future__ import annotations
 
@@ -12,6 +13,7 @@ import re
 import shutil
 import subprocess
 import sys
+import sysconfig
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -20,6 +22,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstencil.so")
 PROBE_LIB = os.path.join(HERE, "libstencil_probe.so")
+# the CPython extension Plan.run calls stencil_apply through (argument marshalling only)
+FASTCALL = os.path.join(HERE, "_fastcall" + (sysconfig.get_config_var("EXT_SUFFIX") or ".so"))
 ARCH = "gfx950"
 
 SOURCES = ["abi.cpp", "kernel_generic.hip", "kernel_stream.hip", "kernel_box.hip", "kernel_star.hip",
@@ -83,16 +87,32 @@ def _link(objs, lib):
     os.replace(tmp, lib)
 
 
+def build_fastcall() -> str:
+    """Compile the CPython extension (gcc) against the built libstencil.so beside it."""
+    tmp = FASTCALL + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-D__HIP_PLATFORM_AMD__", "-I", sysconfig.get_paths()["include"], "-I", INCLUDE,
+           "-I", "/opt/rocm/include", os.path.join(CSRC, "fastcall.c"), "-L", HERE,
+           "-lstencil", "-Wl,-rpath,$ORIGIN", "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("gcc failed for fastcall.c:\n%s\n%s" % (" ".join(cmd), r.stderr))
+    os.replace(tmp, FASTCALL)
+    return FASTCALL
+
+
 def build(verbose: bool = False) -> str:
-    """Compile and link libstencil.so and the copy probe libstencil_probe.so."""
+    """Compile and link libstencil.so, the copy probe libstencil_probe.so and the
+    binding's CPython extension."""
     os.makedirs(BUILD, exist_ok=True)
     srcs = SOURCES + PROBE_SOURCES
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     _link(objs[: len(SOURCES)], LIB)
     _link(objs[len(SOURCES):], PROBE_LIB)
+    build_fastcall()
     if verbose:
-        print("built", LIB, "and", PROBE_LIB)
+        print("built", LIB, PROBE_LIB, "and", FASTCALL)
     return LIB
 
 

@@ -121,3 +121,11 @@ def test_oracle_check_passes_the_oracle_and_fails_a_planted_error(name, dims):
     bad.flat[0] = np.nan
     rec = bench.oracle_check(wl, x, w, k, bad, "test")
     assert not rec["pass"] and rec["nonfinite"] == 1
+
+
+def test_timed_window_of_the_per_workload_legs():
+    assert bench.timed_calls(3.5e-6) == 5000        # launch-bound: capped
+    assert bench.timed_calls(0.125e-3) == 400       # about 50 ms
+    assert bench.timed_calls(0.63e-3) == 79
+    assert bench.timed_calls(10e-3) == 20           # at least 20
+    assert bench.timed_calls(0.0) == 5000
