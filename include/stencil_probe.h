@@ -1,5 +1,5 @@
 /*
- * stencil_probe.h -- HBM probes used to calibrate the stencil measurements.
+ * stencil_probe.h -- HBM and LDS probes used to calibrate the stencil measurements.
  *
  * The stencil kernels are judged against the compulsory-traffic roofline (each input
  * element read once, each output element written once).  This probe measures what a
@@ -41,6 +41,25 @@ int stencil_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t st
  */
 int stencil_probe_triad(const void *a, const void *b, void *dst, int64_t bytes,
                         hipStream_t stream);
+
+/*
+ * stencil_probe_lds -- an LDS access pattern, for the bank-conflict counters: `blocks`
+ * workgroups of 256 threads (4 waves) each hold a 64 KiB LDS buffer; every lane reads
+ * (write = 0, ds_read_b128) or writes (write = 1, ds_write_b128) 16 bytes at byte offset
+ * lane_bytes[lane % 64] of it, 8 x `iters` times.  The eight accesses of an iteration add
+ * 0, 4, ..., 28 KiB to the offset (modulo 64 KiB), which keeps each lane on its own banks,
+ * so the counters of one launch (rocprofv3 --pmc SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT
+ * SQ_LDS_IDX_ACTIVE) describe that one pattern.
+ *   lane_bytes : host array of 64 byte offsets, each a multiple of 16 and at most 65520
+ *                (copied into the kernel arguments; the caller keeps ownership).
+ *   write      : 0 or 1.   iters, blocks : 1 .. 2^20.
+ *   sink       : a device pointer to one float, never written in practice (it keeps the
+ *                compiler from removing the reads).
+ * Asynchronous.  Returns 0 on success, 1 for invalid arguments (checked on the host
+ * before any HIP call), 2 if the launch failed.
+ */
+int stencil_probe_lds(const int32_t *lane_bytes, int32_t write, int32_t iters, int32_t blocks,
+                      float *sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

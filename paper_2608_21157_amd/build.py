@@ -75,7 +75,7 @@ def _compile(src: str) -> str:
     return obj
 
 
-PROBE_SOURCES = ["probe_copy.hip"]
+PROBE_SOURCES = ["probe_copy.hip", "probe_lds.hip"]
 
 
 def _link(objs, lib):
