@@ -12,9 +12,10 @@
 //
 // Nothing in `scratch` must start at zero: a call's weights are in place before its first
 // launch (uploaded, unless the region already holds the same bytes), and the first launch
-// that reads the intermediate grid reads what the launch before it wrote.  Every call on a GPU shares that GPU's array, so calls that overlap
-// in time on one GPU (on different streams, or from different threads without ordering)
-// race on it; calls ordered on one stream do not.
+// that reads the intermediate grid reads what the launch before it wrote.  Every call on
+// a GPU shares that GPU's array, so calls that overlap in time on one GPU (on different
+// streams, or from different threads without ordering) race on it; calls ordered on one
+// stream do not.
 #include <cstring>
 #include <mutex>
 
