@@ -5,8 +5,9 @@
  * Argument marshalling only.  Calling the entry point through ctypes converts every
  * argument on every call (about 1 us per call on the GPU hosts, against 2.5 us for the
  * library's own checks and kernel launch); this module parses ten integers and calls the
- * C function directly.  The library is linked by name with an $ORIGIN run path, so the
- * extension uses the libstencil.so beside it.
+ * C function directly, with the interpreter lock released as ctypes releases it.  The
+ * library is linked by name with an $ORIGIN run path, so the extension uses the
+ * libstencil.so beside it.
  */
 #define PY_SSIZE_T_CLEAN
 #include <Python.h>
@@ -45,9 +46,13 @@ static PyObject *fastcall_apply(PyObject *self, PyObject *const *args, Py_ssize_
         PyErr_SetString(PyExc_OverflowError, "radius, boundary and steps must fit int32");
         return NULL;
     }
-    const stencil_status st =
-        stencil_apply((stencil_plan_t)p[0], p[1], p[2], (const int64_t *)p[3], p[4], p[5],
-                      (int32_t)radius, (int32_t)boundary, (int32_t)steps, (hipStream_t)p[6]);
+    /* the interpreter lock is released during the call, as ctypes does, so that calls
+     * from several threads (on different plans) overlap */
+    stencil_status st;
+    Py_BEGIN_ALLOW_THREADS
+    st = stencil_apply((stencil_plan_t)p[0], p[1], p[2], (const int64_t *)p[3], p[4], p[5],
+                       (int32_t)radius, (int32_t)boundary, (int32_t)steps, (hipStream_t)p[6]);
+    Py_END_ALLOW_THREADS
     return PyLong_FromLong((long)st);
 }
 

@@ -1,5 +1,5 @@
 """Independent plans used at the same time: each on its own stream, interleaved from one
-host thread, and from two host threads at once (ctypes releases the GIL during each
+host thread, and from two host threads at once (the binding releases the GIL during each
 library call, so the calls really overlap).  A plan holds all of its mutable state (its
 buffers, its weights, its launch choice); the library's only shared state is the
 thread-local error string and the per-kernel occupancy counts computed once.  Every
