@@ -271,24 +271,40 @@ __global__ __launch_bounds__((Tb2Shape<T, R, PF>::THREADS)) void stencil_star_tb
 #pragma unroll
         for (int i = 0; i < R; ++i)
             gb[i] = buf[idx + (i + 1) * pitch];
+        // x: the row of scalars from HXV vectors left to HXV vectors right.  Where the
+        // reach is shorter than a vector only the R elements next to the centre vector are
+        // read on each side (one ds_read2 of 4 or 8 bytes per side pair instead of two
+        // 16-byte reads)
+        constexpr bool NARROW = HXV == 1 && R < VEC;
+        T xs[(2 * HXV + 1) * VEC];
+        if constexpr (NARROW) {
+            const T *fb = reinterpret_cast<const T *>(buf);
 #pragma unroll
-        for (int k = 0; k < HXV; ++k) {
-            gb[R + k] = buf[idx - HXV + k];
-            gb[R + HXV + k] = buf[idx + 1 + k];
+            for (int e = VEC - R; e < VEC; ++e)
+                xs[e] = fb[(idx - 1) * VEC + e];
+#pragma unroll
+            for (int e = 0; e < R; ++e)
+                xs[2 * VEC + e] = fb[(idx + 1) * VEC + e];
+        } else {
+#pragma unroll
+            for (int k = 0; k < HXV; ++k) {
+                gb[R + k] = buf[idx - HXV + k];
+                gb[R + HXV + k] = buf[idx + 1 + k];
+            }
         }
 #pragma unroll
         for (int i = 0; i < R; ++i)
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
                 acc[e] = fma(wy[R + i], gb[i].e[e], acc[e]);
-        // x: the row of scalars from HXV vectors left to HXV vectors right
-        T xs[(2 * HXV + 1) * VEC];
+        if constexpr (!NARROW) {
 #pragma unroll
-        for (int k = 0; k < HXV; ++k) {
+            for (int k = 0; k < HXV; ++k) {
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                xs[k * VEC + e] = gb[R + k].e[e];
-                xs[(HXV + 1 + k) * VEC + e] = gb[R + HXV + k].e[e];
+                for (int e = 0; e < VEC; ++e) {
+                    xs[k * VEC + e] = gb[R + k].e[e];
+                    xs[(HXV + 1 + k) * VEC + e] = gb[R + HXV + k].e[e];
+                }
             }
         }
 #pragma unroll
