@@ -381,6 +381,20 @@ def test_box3_z_chunks_both_directions(name, gs):
            tolerance(wl, x, k))
 
 
+@pytest.mark.parametrize("gs", [-1, 0, 1], ids=["s-1", "s0", "s1"])
+def test_star_fused_z_chunks(gs):
+    """The fused star's z chunking at radius 1 on 203 x 256^2, two steps: grid scale 0 is
+    one workgroup per CU in 26-plane chunks (a round of two per CU would give 13-plane
+    chunks), +1 that former round, -1 51-plane chunks; the last chunk of each is short and
+    odd chunks stream downwards.  Every point against the oracle."""
+    wl, (x, w, k) = _case("c2", (203, 256, 256), None, 2)
+    print("[case] star fused z chunks dims=%s grid_scale=%d" % (wl.dims, gs), flush=True)
+    got, info = run_library(wl, x, w, k, grid_scale=gs)
+    assert info["kernel"] == "stencil_star_tb2_kernel", info
+    report("star chunks s%d %s" % (gs, info), got, oracle_full(wl, x, w, k),
+           tolerance(wl, x, k))
+
+
 RADIUS0 = [(B.STAR, 3, B.ZERO, False), (B.BOX, 3, B.PERIODIC, True),
            (B.BOX, 2, B.ZERO, False), (B.STAR, 2, B.PERIODIC, False)]
 
