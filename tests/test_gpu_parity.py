@@ -175,6 +175,33 @@ def test_nondefault_stream():
     report("stream", got, ref, tolerance(wl, x, k))
 
 
+def test_run_without_a_stream_follows_torchs_current_stream():
+    """Plan.run with no stream launches on torch's current stream, resolved again on every
+    call: two side streams are made current in turn, each first spins (torch.cuda._sleep)
+    and then writes the input, so a launch on any other stream would read the input
+    before it is written.  Both calls must match the oracle."""
+    wl, (x, w, k) = _case("c3", (16, 20, 264), None, 2)
+    ref = oracle_full(wl, x, w, k)
+    src = torch.from_numpy(x).to(torch.device("cuda:0"))
+    torch.cuda.synchronize()
+    plan = B.Plan(B.make_desc(wl.ndim, wl.dims, shape=wl.shape, radius=wl.radius,
+                              boundary=wl.boundary))
+    try:
+        for round_ in range(2):
+            side = torch.cuda.Stream()
+            with torch.cuda.stream(side):
+                xt = torch.zeros_like(src)
+                yt = torch.full_like(src, float("nan"))
+                torch.cuda._sleep(20_000_000)
+                xt.copy_(src)
+                plan.run(xt, yt, w, steps=wl.steps)
+            side.synchronize()
+            report("current stream %d" % round_, yt.cpu().numpy().astype(np.float64), ref,
+                   tolerance(wl, x, k))
+    finally:
+        plan.close()
+
+
 def test_variants_agree():
     """Every variant the planner can force gives the oracle's result on the same input."""
     wl, (x, w, k) = _case("c4", (16, 20, 512), None, None)
