@@ -162,8 +162,9 @@ stencil_status stencil_plan(const stencil_desc *desc, stencil_plan_t *out_plan);
  * Ownership: in, out and coeff_field belong to the caller and must stay valid until the
  * stream work completes.  Asynchronous: returns once the work is enqueued.  Calls on one
  * plan must be ordered on one stream at a time (the plan's ping-pong grid and coefficient
- * buffer are reused).  Pointers or x extents that do not meet a fast kernel's alignment
- * select a slower kernel; they are not an error.
+ * buffer are reused), and one plan must not be called from several host threads at once;
+ * different plans may be used concurrently.  Pointers or x extents that do not meet a
+ * fast kernel's alignment select a slower kernel; they are not an error.
  * Returns STENCIL_OK, INVALID_ARG, MISMATCH, ALIAS, NO_MEMORY or ERR_HIP.
  */
 stencil_status stencil_apply(stencil_plan_t plan, const void *in, void *out,

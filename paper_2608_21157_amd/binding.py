@@ -213,7 +213,9 @@ class Plan:
     is called.  The objects last validated are held until another one is passed (or the
     plan is closed), so an unchanged object is not checked again; resizing a validated
     tensor in place between calls is not detected.  Weight values changed in place are
-    still seen: the library compares the weights' bytes on every call."""
+    still seen: the library compares the weights' bytes on every call.  A Plan is used
+    from one thread at a time (its cached arguments and the plan's buffers are shared
+    state); separate Plans may run on separate threads and streams."""
 
     def __init__(self, desc: StencilDesc):
         self.desc = desc
